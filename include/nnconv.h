@@ -1,0 +1,159 @@
+/*
+ * nnconv.h -- C ABI of libnnconv: mixed-precision 2-D convolution in the
+ * three training passes (forward, backward-data, backward-weight) on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the paper's convolution call (Sec. 3.2, Listings 4-5:
+ * convolution(x, base_axis=1, outmaps, kernel, ...)), trained by
+ * back-propagation (Sec. 2.1) in mixed precision: half-precision storage of
+ * weights, activations and gradients, products accumulated in fp32, and a
+ * loss scale S that multiplies the incoming gradient and is divided out of
+ * the weight gradient before the fp32 update (Sec. 3.3, Listing 6).
+ *
+ * Definitions (cross-correlation, symmetric zero padding):
+ *   P = floor((H + 2*pad_h - dil_h*(R-1) - 1) / stride_h) + 1   (same for Q)
+ *   Cg = C/groups, Kg = K/groups; output channel k reads input channels
+ *   [ (k/Kg)*Cg, (k/Kg)*Cg + Cg ).
+ *   forward   y[n,k,p,q]  = alpha * sum_{c<Cg,r<R,s<S} xz[n,(k/Kg)*Cg+c, p*sh-ph+r*dh, q*sw-pw+s*dw] * w[k,c,r,s]
+ *   dgrad     dx = alpha * (adjoint of the forward map in x) applied to dy
+ *   wgrad     dw = beta * dw + inv_loss_scale * (adjoint of the forward map in w)(x, dy)
+ *   where xz is x extended by zeros.  dy is expected to carry the loss scale
+ *   already (the caller scaled the loss); dgrad keeps it, wgrad removes it.
+ *
+ * Layouts (dense, contiguous):
+ *   NNCONV_NCHW  x[N][C][H][W], y/dy[N][K][P][Q], w/dw[K][Cg][R][S]
+ *   NNCONV_NHWC  x[N][H][W][C], y/dy[N][P][Q][K], w/dw[K][R][S][Cg]
+ *
+ * Ownership and execution:
+ *   - Every buffer is a device pointer owned by the caller; the library
+ *     allocates no memory (scratch comes from the caller's workspace, sized
+ *     by nnconv_workspace_size) and never synchronises.
+ *   - Work is queued on the caller's HIP stream (hipStream_t passed as
+ *     void*; NULL means the default stream).  Calls return once queued.
+ *   - The library keeps no mutable global state: calls are reentrant, and
+ *     calls on different streams with disjoint buffers may run concurrently.
+ *   - Fast (matrix-core) paths need 16-byte aligned pointers and Cg, Kg that
+ *     are multiples of 8; other valid shapes run on slower direct kernels
+ *     with identical semantics.
+ *
+ * Errors: every argument check happens on the host before anything is
+ * queued.  On a non-OK status nothing is launched and no output or
+ * workspace byte is touched.  No exception crosses the ABI and nothing is
+ * printed.
+ */
+#ifndef NNCONV_H
+#define NNCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define NNCONV_VERSION 1
+
+typedef enum {
+    NNCONV_OK = 0,
+    NNCONV_ERR_INVALID_ARG = 1,   /* bad shape, null pointer, bad enum */
+    NNCONV_ERR_UNSUPPORTED = 2,   /* valid but not provided (e.g. dtype combination) */
+    NNCONV_ERR_WORKSPACE = 3,     /* ws_bytes smaller than nnconv_workspace_size() */
+    NNCONV_ERR_MISALIGNED = 4,    /* pointer alignment below the element size */
+    NNCONV_ERR_HIP = 5            /* the HIP runtime refused a launch */
+} nnconv_status;
+
+typedef enum { NNCONV_NCHW = 0, NNCONV_NHWC = 1 } nnconv_layout;
+typedef enum { NNCONV_F16 = 0, NNCONV_BF16 = 1, NNCONV_F32 = 2 } nnconv_dtype;
+typedef enum { NNCONV_FWD = 0, NNCONV_DGRAD = 1, NNCONV_WGRAD = 2 } nnconv_pass;
+
+/* Convolution geometry (the parameters of the paper's convolution call plus
+ * stride, padding, dilation, groups, layout and operand type). */
+typedef struct {
+    int32_t n, c, h, w;          /* batch, input channels, input height, width */
+    int32_t k, r, s;             /* output channels, filter height, width */
+    int32_t stride_h, stride_w;  /* >= 1 */
+    int32_t pad_h, pad_w;        /* >= 0, zero padding on both sides */
+    int32_t dil_h, dil_w;        /* >= 1 */
+    int32_t groups;              /* >= 1, divides c and k */
+    int32_t layout;              /* nnconv_layout */
+    int32_t dtype;               /* nnconv_dtype of x, w, y, dy, dx: F16 or BF16 */
+} nnconv_desc;
+
+/* Library version (NNCONV_VERSION). */
+int32_t nnconv_version(void);
+
+/* The hipError_t code behind the most recent NNCONV_ERR_HIP returned on the
+ * calling thread (0 if there was none). */
+int32_t nnconv_last_hip_error(void);
+
+/* Static, human-readable name of a status code. */
+const char *nnconv_status_string(nnconv_status status);
+
+/* Output size (P, Q) from the floor formula above.
+ * INVALID_ARG for a null argument, non-positive sizes, negative padding,
+ * groups not dividing c and k, or an empty output. */
+nnconv_status nnconv_output_dims(const nnconv_desc *desc, int32_t *p, int32_t *q);
+
+/* Bytes of device workspace that nnconv_fwd / nnconv_dgrad / nnconv_wgrad
+ * need for this geometry (0 is a valid answer).  Depends only on desc and
+ * pass.  Workspace contents need not be initialised and are garbage after
+ * the call. */
+nnconv_status nnconv_workspace_size(const nnconv_desc *desc, nnconv_pass pass, size_t *bytes);
+
+/* Forward pass (definition above): y = alpha * conv(x, w).
+ * x, w, y: device pointers in desc->layout, element type desc->dtype.
+ * Accumulation in fp32; y is rounded to nearest-even once, overflow gives
+ * +-inf.  y must not overlap x, w or ws. */
+nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, const void *w, void *y,
+                         float alpha, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* Backward-data pass: dx = alpha * (adjoint in x)(dy).  dy carries the
+ * loss scale and dx keeps it.  Input positions that no output reads get an
+ * exact 0.  dx must not overlap dy, w or ws. */
+nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, const void *w, void *dx,
+                           float alpha, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* Backward-weight pass with the loss-scale step of Sec. 3.3 / Listing 6:
+ *   dw = (accumulate ? dw : 0) + inv_loss_scale * sum_{n,p,q} dy * xz
+ * The batch-pixel reduction is split over the workspace in fp32 and summed
+ * in a fixed order, so results are bitwise reproducible.
+ * dw_dtype: NNCONV_F32 (for fp32 master weights) or desc->dtype.
+ * accumulate: 0 overwrites dw (its old contents are not read), 1 adds.
+ * overflow_flag: NULL or a device int32 that the caller zeroed; the call
+ *   stores 1 into it when any final dw element is inf or NaN and never
+ *   clears it (one flag can cover every layer of a step, as
+ *   check_inf_or_nan_grad does in Listing 6). */
+nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, const void *dy, void *dw,
+                           int32_t dw_dtype, float inv_loss_scale, int32_t accumulate,
+                           int32_t *overflow_flag, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* Layout transforms (pure data movement of 16-bit elements, bit exact).
+ *
+ * Activations: src[N][C][H][W] -> dst[N][H][W][c_pad], c_pad >= C; channels
+ * C..c_pad-1 of dst are zero (the stem's 3 channels padded to 8). */
+nnconv_status nnconv_nchw_to_nhwc(const void *src, void *dst, int32_t n, int32_t c, int32_t h,
+                                  int32_t w, int32_t c_pad, void *hip_stream);
+
+/* Activations: src[N][H][W][C] -> dst[N][C][H][W]. */
+nnconv_status nnconv_nhwc_to_nchw(const void *src, void *dst, int32_t n, int32_t c, int32_t h,
+                                  int32_t w, void *hip_stream);
+
+/* Channel padding in channel-last form: src[rows][c] -> dst[rows][c_pad],
+ * extra channels zero (rows = N*H*W). */
+nnconv_status nnconv_pad_channels(const void *src, void *dst, int64_t rows, int32_t c,
+                                  int32_t c_pad, void *hip_stream);
+
+/* Weights: src[K][Cg][R][S] -> dst[K][R][S][cg_pad], cg_pad >= Cg, padding
+ * zero. */
+nnconv_status nnconv_weight_kcrs_to_krsc(const void *src, void *dst, int32_t k, int32_t cg,
+                                         int32_t r, int32_t s, int32_t cg_pad, void *hip_stream);
+
+/* Weights: src[K][R][S][Cg] -> dst[K][Cg][R][S]. */
+nnconv_status nnconv_weight_krsc_to_kcrs(const void *src, void *dst, int32_t k, int32_t cg,
+                                         int32_t r, int32_t s, void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NNCONV_H */

@@ -1,0 +1,541 @@
+// api.hip -- the C ABI of libnnconv: argument validation (host only, before
+// anything is queued), workspace planning, and dispatch to the kernels.
+#include "nnconv.h"
+
+#include <string.h>
+
+#include "launch.hpp"
+
+#define NNCONV_API extern "C" __attribute__((visibility("default")))
+
+using namespace nnconv;
+
+namespace {
+
+struct Geom {
+    int64_t n, c, h, w, k, r, s, sh, sw, ph, pw, dh, dw, g, p, q, cg, kg;
+    int layout, dtype;
+};
+
+constexpr int64_t MAX_ELEMS = int64_t(1) << 40;
+
+nnconv_status validate(const nnconv_desc *d, Geom *G) {
+    if (!d) return NNCONV_ERR_INVALID_ARG;
+    if (d->n < 1 || d->c < 1 || d->h < 1 || d->w < 1 || d->k < 1 || d->r < 1 || d->s < 1)
+        return NNCONV_ERR_INVALID_ARG;
+    if (d->stride_h < 1 || d->stride_w < 1 || d->dil_h < 1 || d->dil_w < 1 || d->pad_h < 0 ||
+        d->pad_w < 0 || d->groups < 1)
+        return NNCONV_ERR_INVALID_ARG;
+    if (d->c % d->groups != 0 || d->k % d->groups != 0) return NNCONV_ERR_INVALID_ARG;
+    if (d->layout != NNCONV_NCHW && d->layout != NNCONV_NHWC) return NNCONV_ERR_INVALID_ARG;
+    if (d->dtype != NNCONV_F16 && d->dtype != NNCONV_BF16) {
+        if (d->dtype == NNCONV_F32) return NNCONV_ERR_UNSUPPORTED;
+        return NNCONV_ERR_INVALID_ARG;
+    }
+    Geom g;
+    g.n = d->n; g.c = d->c; g.h = d->h; g.w = d->w; g.k = d->k; g.r = d->r; g.s = d->s;
+    g.sh = d->stride_h; g.sw = d->stride_w; g.ph = d->pad_h; g.pw = d->pad_w;
+    g.dh = d->dil_h; g.dw = d->dil_w; g.g = d->groups;
+    const int64_t num_h = g.h + 2 * g.ph - g.dh * (g.r - 1) - 1;
+    const int64_t num_w = g.w + 2 * g.pw - g.dw * (g.s - 1) - 1;
+    if (num_h < 0 || num_w < 0) return NNCONV_ERR_INVALID_ARG;
+    g.p = num_h / g.sh + 1;
+    g.q = num_w / g.sw + 1;
+    g.cg = g.c / g.g;
+    g.kg = g.k / g.g;
+    // guard the size products used below
+    if (g.n * g.c > MAX_ELEMS / (g.h * g.w) || g.n * g.k > MAX_ELEMS / (g.p * g.q) ||
+        g.k * g.cg > MAX_ELEMS / (g.r * g.s))
+        return NNCONV_ERR_INVALID_ARG;
+    g.layout = d->layout;
+    g.dtype = d->dtype;
+    *G = g;
+    return NNCONV_OK;
+}
+
+inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+inline bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Shape-level eligibility of the matrix-core path.
+bool fast_shape(const Geom &G) {
+    if (G.cg % 8 != 0 || G.kg % 8 != 0) return false;
+    if (G.r * G.s > MAX_TAPS) return false;
+    const int64_t lim = MAX_BUFFER_BYTES / 2;  // elements per operand
+    if (G.n * G.h * G.w * G.c > lim) return false;
+    if (G.n * G.p * G.q * G.k > lim) return false;
+    if (G.k * G.r * G.s * G.cg > lim) return false;
+    return true;
+}
+
+// ---------------------------------------------------------------------------
+// planning: workspace regions and split counts (pure functions of the shape)
+// ---------------------------------------------------------------------------
+
+struct WgPlan {
+    WGConfig cfg;
+    int32_t splits, pix_per_split;
+};
+
+WgPlan plan_wgrad_fast(const Geom &G) {
+    WgPlan pl;
+    const int64_t bmk = G.kg <= 64 ? 64 : 128, bnj = 128;
+    pl.cfg = G.kg <= 64 ? WG_64x128 : WG_128x128;
+    const int64_t rscg = G.r * G.s * G.cg;
+    const int64_t tiles = G.g * ((G.kg + bmk - 1) / bmk) * ((rscg + bnj - 1) / bnj);
+    const int64_t npq = G.n * G.p * G.q;
+    const int64_t iters = (npq + 63) / 64;
+    int64_t splits = (512 + tiles - 1) / tiles;
+    int64_t max_splits = iters / 4;  // at least 4 pixel slices per split
+    if (max_splits < 1) max_splits = 1;
+    if (splits > max_splits) splits = max_splits;
+    if (splits > 1024) splits = 1024;
+    if (splits < 1) splits = 1;
+    const int64_t per = ((iters + splits - 1) / splits) * 64;
+    pl.pix_per_split = (int32_t)per;
+    pl.splits = (int32_t)((npq + per - 1) / per);
+    return pl;
+}
+
+int32_t plan_wgrad_direct_splits(const Geom &G) {
+    const int64_t npq = G.n * G.p * G.q;
+    int64_t s = (npq + 2047) / 2048;
+    if (s > 64) s = 64;
+    if (s < 1) s = 1;
+    return (int32_t)s;
+}
+
+struct Regions {  // byte offsets into the caller's workspace
+    size_t a, b, c, d, total;
+};
+
+Regions fast_regions(const Geom &G, nnconv_pass pass) {
+    Regions R = {0, 0, 0, 0, 0};
+    const size_t e2 = 2;
+    const size_t xb = G.n * G.h * G.w * G.c * e2;
+    const size_t yb = G.n * G.p * G.q * G.k * e2;
+    const size_t wb = G.k * G.r * G.s * G.cg * e2;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    const bool nchw = G.layout == NNCONV_NCHW;
+    if (pass == NNCONV_FWD) {
+        if (nchw) {
+            R.a = take(xb);  // x channel-last
+            R.b = take(wb);  // w [K][R][S][Cg]
+            R.c = take(yb);  // y channel-last
+        }
+    } else if (pass == NNCONV_DGRAD) {
+        if (nchw) {
+            R.a = take(yb);  // dy channel-last
+            R.d = take(wb);  // w [K][R][S][Cg] (intermediate)
+            R.c = take(xb);  // dx channel-last
+        }
+        R.b = take(wb);      // w [g][R][S][Cg][Kg]
+    } else {
+        if (nchw) {
+            R.a = take(xb);  // x channel-last
+            R.b = take(yb);  // dy channel-last
+        }
+        const WgPlan pl = plan_wgrad_fast(G);
+        R.c = take((size_t)pl.splits * G.k * G.r * G.s * G.cg * 4);
+    }
+    R.total = off;
+    return R;
+}
+
+size_t direct_ws(const Geom &G, nnconv_pass pass) {
+    if (pass != NNCONV_WGRAD) return 0;
+    return align256((size_t)plan_wgrad_direct_splits(G) * G.k * G.r * G.s * G.cg * 4);
+}
+
+size_t workspace_bytes(const Geom &G, nnconv_pass pass) {
+    size_t d = direct_ws(G, pass);
+    if (!fast_shape(G)) return d;
+    size_t f = fast_regions(G, pass).total;
+    return f > d ? f : d;
+}
+
+DirectParams direct_params(const Geom &G, float alpha) {
+    DirectParams P;
+    P.n = (int32_t)G.n; P.c = (int32_t)G.c; P.h = (int32_t)G.h; P.w = (int32_t)G.w;
+    P.k = (int32_t)G.k; P.r = (int32_t)G.r; P.s = (int32_t)G.s; P.p = (int32_t)G.p;
+    P.q = (int32_t)G.q; P.sh = (int32_t)G.sh; P.sw = (int32_t)G.sw; P.ph = (int32_t)G.ph;
+    P.pw = (int32_t)G.pw; P.dh = (int32_t)G.dh; P.dw = (int32_t)G.dw;
+    P.groups = (int32_t)G.g; P.cg = (int32_t)G.cg; P.kg = (int32_t)G.kg;
+    if (G.layout == NNCONV_NCHW) {
+        P.xs[0] = G.c * G.h * G.w; P.xs[1] = G.h * G.w; P.xs[2] = G.w; P.xs[3] = 1;
+        P.ys[0] = G.k * G.p * G.q; P.ys[1] = G.p * G.q; P.ys[2] = G.q; P.ys[3] = 1;
+        P.wsd[0] = G.cg * G.r * G.s; P.wsd[1] = G.r * G.s; P.wsd[2] = G.s; P.wsd[3] = 1;
+    } else {
+        P.xs[0] = G.h * G.w * G.c; P.xs[1] = 1; P.xs[2] = G.w * G.c; P.xs[3] = G.c;
+        P.ys[0] = G.p * G.q * G.k; P.ys[1] = 1; P.ys[2] = G.q * G.k; P.ys[3] = G.k;
+        P.wsd[0] = G.r * G.s * G.cg; P.wsd[1] = 1; P.wsd[2] = G.s * G.cg; P.wsd[3] = G.cg;
+    }
+    P.alpha = alpha;
+    return P;
+}
+
+thread_local int32_t last_hip_error = 0;
+
+inline nnconv_status hip_status(hipError_t e) {
+    if (e == hipSuccess) return NNCONV_OK;
+    last_hip_error = (int32_t)e;
+    return NNCONV_ERR_HIP;
+}
+
+#define TRY_HIP(expr)                                          \
+    do {                                                       \
+        hipError_t e_ = (expr);                                \
+        if (e_ != hipSuccess) return hip_status(e_);           \
+    } while (0)
+
+// Launch errors are read with hipGetLastError; drop any error an unrelated
+// earlier runtime call on this thread left behind so it is not blamed on us.
+inline void clear_stale_error() { (void)hipGetLastError(); }
+
+// Common part of the forward pass and of each backward-data phase.
+TNParams tn_base() {
+    TNParams p;
+    memset(&p, 0, sizeof(p));
+    return p;
+}
+
+TNConfig pick_tn(int64_t ncols) { return ncols <= 64 ? TN_256x64 : TN_128x128; }
+
+nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
+                       hipStream_t st) {
+    TNParams p = tn_base();
+    p.a = x;
+    p.a_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+    p.b = w;
+    p.b_bytes = (uint32_t)(G.k * G.r * G.s * G.cg * 2);
+    p.out = y;
+    p.mi = (int32_t)G.p;
+    p.mj = (int32_t)G.q;
+    p.M = (int32_t)(G.n * G.p * G.q);
+    p.div_mj = make_fastdiv((uint32_t)G.q);
+    p.div_mi = make_fastdiv((uint32_t)G.p);
+    p.a_h = (int32_t)G.h; p.a_w = (int32_t)G.w; p.a_c = (int32_t)G.c;
+    p.a_cg_ofs = (int32_t)G.cg;
+    p.ai_mul = (int32_t)G.sh; p.ai_add = (int32_t)-G.ph;
+    p.aj_mul = (int32_t)G.sw; p.aj_add = (int32_t)-G.pw;
+    p.cr = (int32_t)G.cg;
+    p.div_crv = make_fastdiv((uint32_t)(G.cg / 8));
+    p.ncols = (int32_t)G.kg;
+    p.b_ld = (int32_t)(G.r * G.s * G.cg);
+    p.b_g_ofs = (int32_t)(G.kg * G.r * G.s * G.cg);
+    p.o_h = (int32_t)G.p; p.o_w = (int32_t)G.q; p.o_c = (int32_t)G.k;
+    p.o_cg_ofs = (int32_t)G.kg;
+    p.oi_mul = 1; p.oi_add = 0; p.oj_mul = 1; p.oj_add = 0;
+    p.alpha = alpha;
+    p.groups = (int32_t)G.g;
+    int t = 0;
+    for (int r = 0; r < G.r; ++r)
+        for (int s = 0; s < G.s; ++s, ++t) {
+            p.taps.dh[t] = (int32_t)(r * G.dh);
+            p.taps.dw[t] = (int32_t)(s * G.dw);
+            p.taps.boff[t] = (int32_t)(t * G.cg);
+        }
+    p.taps.n = t;
+    p.k_iters = (int32_t)((int64_t(t) * G.cg + 63) / 64);
+    return hip_status(launch_igemm_tn(G.dtype, pick_tn(G.kg), p, st));
+}
+
+// Backward-data as sigma_h * sigma_w independent implicit GEMMs, one per
+// output phase (h mod sigma_h, w mod sigma_w): within a phase every pixel
+// sees the same set of contributing taps.  wt is [g][R][S][Cg][Kg].
+nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx, float alpha,
+                         hipStream_t st) {
+    for (int64_t phh = 0; phh < G.sh; ++phh) {
+        for (int64_t phw = 0; phw < G.sw; ++phw) {
+            const int64_t mi = phh < G.h ? (G.h - phh + G.sh - 1) / G.sh : 0;
+            const int64_t mj = phw < G.w ? (G.w - phw + G.sw - 1) / G.sw : 0;
+            if (mi == 0 || mj == 0) continue;
+            TNParams p = tn_base();
+            p.a = dy;
+            p.a_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
+            p.b = wt;
+            p.b_bytes = (uint32_t)(G.k * G.r * G.s * G.cg * 2);
+            p.out = dx;
+            p.mi = (int32_t)mi;
+            p.mj = (int32_t)mj;
+            p.M = (int32_t)(G.n * mi * mj);
+            p.div_mj = make_fastdiv((uint32_t)mj);
+            p.div_mi = make_fastdiv((uint32_t)mi);
+            p.a_h = (int32_t)G.p; p.a_w = (int32_t)G.q; p.a_c = (int32_t)G.k;
+            p.a_cg_ofs = (int32_t)G.kg;
+            p.ai_mul = 1; p.ai_add = 0; p.aj_mul = 1; p.aj_add = 0;
+            p.cr = (int32_t)G.kg;
+            p.div_crv = make_fastdiv((uint32_t)(G.kg / 8));
+            p.ncols = (int32_t)G.cg;
+            p.b_ld = (int32_t)G.kg;
+            p.b_g_ofs = (int32_t)(G.r * G.s * G.cg * G.kg);
+            p.o_h = (int32_t)G.h; p.o_w = (int32_t)G.w; p.o_c = (int32_t)G.c;
+            p.o_cg_ofs = (int32_t)G.cg;
+            p.oi_mul = (int32_t)G.sh; p.oi_add = (int32_t)phh;
+            p.oj_mul = (int32_t)G.sw; p.oj_add = (int32_t)phw;
+            p.alpha = alpha;
+            p.groups = (int32_t)G.g;
+            int t = 0;
+            for (int64_t r = 0; r < G.r; ++r) {
+                const int64_t nh = phh + G.ph - r * G.dh;  // = sigma_h * (p - i)
+                if (((nh % G.sh) + G.sh) % G.sh != 0) continue;
+                for (int64_t s = 0; s < G.s; ++s) {
+                    const int64_t nw = phw + G.pw - s * G.dw;
+                    if (((nw % G.sw) + G.sw) % G.sw != 0) continue;
+                    p.taps.dh[t] = (int32_t)(nh / G.sh);
+                    p.taps.dw[t] = (int32_t)(nw / G.sw);
+                    p.taps.boff[t] = (int32_t)((r * G.s + s) * G.cg * G.kg);
+                    ++t;
+                }
+            }
+            p.taps.n = t;
+            p.k_iters = (int32_t)((int64_t(t) * G.kg + 63) / 64);
+            TRY_HIP(launch_igemm_tn(G.dtype, pick_tn(G.cg), p, st));
+        }
+    }
+    return NNCONV_OK;
+}
+
+nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *part,
+                         hipStream_t st) {
+    const WgPlan pl = plan_wgrad_fast(G);
+    WGParams p;
+    memset(&p, 0, sizeof(p));
+    p.x = x;
+    p.x_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+    p.dy = dy;
+    p.dy_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
+    p.ws = part;
+    p.h = (int32_t)G.h; p.w = (int32_t)G.w; p.c = (int32_t)G.c; p.k = (int32_t)G.k;
+    p.cg = (int32_t)G.cg; p.kg = (int32_t)G.kg;
+    p.p = (int32_t)G.p; p.q = (int32_t)G.q; p.npq = (int32_t)(G.n * G.p * G.q);
+    p.div_q = make_fastdiv((uint32_t)G.q);
+    p.div_pq = make_fastdiv((uint32_t)(G.p * G.q));
+    p.div_cg = make_fastdiv((uint32_t)G.cg);
+    p.div_s = make_fastdiv((uint32_t)G.s);
+    p.sh = (int32_t)G.sh; p.sw = (int32_t)G.sw; p.ph = (int32_t)G.ph; p.pw = (int32_t)G.pw;
+    p.dh = (int32_t)G.dh; p.dw = (int32_t)G.dw;
+    p.rscg = (int32_t)(G.r * G.s * G.cg);
+    p.groups = (int32_t)G.g;
+    p.splits = pl.splits;
+    p.pix_per_split = pl.pix_per_split;
+    TRY_HIP(launch_wgrad_splitk(G.dtype, pl.cfg, p, st));
+    return NNCONV_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// exported entry points
+// ---------------------------------------------------------------------------
+
+NNCONV_API int32_t nnconv_version(void) { return NNCONV_VERSION; }
+
+NNCONV_API int32_t nnconv_last_hip_error(void) { return last_hip_error; }
+
+NNCONV_API const char *nnconv_status_string(nnconv_status s) {
+    switch (s) {
+        case NNCONV_OK: return "ok";
+        case NNCONV_ERR_INVALID_ARG: return "invalid argument";
+        case NNCONV_ERR_UNSUPPORTED: return "unsupported";
+        case NNCONV_ERR_WORKSPACE: return "workspace too small";
+        case NNCONV_ERR_MISALIGNED: return "misaligned pointer";
+        case NNCONV_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+NNCONV_API nnconv_status nnconv_output_dims(const nnconv_desc *desc, int32_t *p, int32_t *q) {
+    if (!p || !q) return NNCONV_ERR_INVALID_ARG;
+    Geom G;
+    nnconv_status st = validate(desc, &G);
+    if (st != NNCONV_OK) return st;
+    *p = (int32_t)G.p;
+    *q = (int32_t)G.q;
+    return NNCONV_OK;
+}
+
+NNCONV_API nnconv_status nnconv_workspace_size(const nnconv_desc *desc, nnconv_pass pass,
+                                               size_t *bytes) {
+    if (!bytes) return NNCONV_ERR_INVALID_ARG;
+    if (pass != NNCONV_FWD && pass != NNCONV_DGRAD && pass != NNCONV_WGRAD)
+        return NNCONV_ERR_INVALID_ARG;
+    Geom G;
+    nnconv_status st = validate(desc, &G);
+    if (st != NNCONV_OK) return st;
+    *bytes = workspace_bytes(G, pass);
+    return NNCONV_OK;
+}
+
+static nnconv_status check_ws(const Geom &G, nnconv_pass pass, const void *ws, size_t ws_bytes) {
+    const size_t need = workspace_bytes(G, pass);
+    if (ws_bytes < need) return NNCONV_ERR_WORKSPACE;
+    if (need > 0 && !ws) return NNCONV_ERR_INVALID_ARG;
+    return NNCONV_OK;
+}
+
+NNCONV_API nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, const void *w, void *y,
+                                    float alpha, void *ws, size_t ws_bytes, void *hip_stream) {
+    Geom G;
+    nnconv_status st = validate(desc, &G);
+    if (st != NNCONV_OK) return st;
+    if (!x || !w || !y) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(x, 2) || !aligned(w, 2) || !aligned(y, 2)) return NNCONV_ERR_MISALIGNED;
+    if ((st = check_ws(G, NNCONV_FWD, ws, ws_bytes)) != NNCONV_OK) return st;
+    hipStream_t s = (hipStream_t)hip_stream;
+    clear_stale_error();
+    const bool fast = fast_shape(G) && aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
+                      (G.layout == NNCONV_NHWC || aligned(ws, 16));
+    if (!fast) return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
+    if (G.layout == NNCONV_NHWC) return fwd_fast(G, x, w, y, alpha, s);
+    const Regions R = fast_regions(G, NNCONV_FWD);
+    char *base = (char *)ws;
+    void *xt = base + R.a, *wt = base + R.b, *yt = base + R.c;
+    TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, s));
+    TRY_HIP(launch_transpose16(w, wt, G.k, G.cg, G.r * G.s, G.cg, s));
+    if ((st = fwd_fast(G, xt, wt, yt, alpha, s)) != NNCONV_OK) return st;
+    return hip_status(launch_transpose16(yt, y, G.n, G.p * G.q, G.k, G.p * G.q, s));
+}
+
+NNCONV_API nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, const void *w,
+                                      void *dx, float alpha, void *ws, size_t ws_bytes,
+                                      void *hip_stream) {
+    Geom G;
+    nnconv_status st = validate(desc, &G);
+    if (st != NNCONV_OK) return st;
+    if (!dy || !w || !dx) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(dy, 2) || !aligned(w, 2) || !aligned(dx, 2)) return NNCONV_ERR_MISALIGNED;
+    if ((st = check_ws(G, NNCONV_DGRAD, ws, ws_bytes)) != NNCONV_OK) return st;
+    hipStream_t s = (hipStream_t)hip_stream;
+    clear_stale_error();
+    const bool fast = fast_shape(G) && aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
+                      aligned(ws, 16);
+    if (!fast)
+        return hip_status(launch_direct_dgrad(G.dtype, direct_params(G, alpha), dy, w, dx, s));
+    const Regions R = fast_regions(G, NNCONV_DGRAD);
+    char *base = (char *)ws;
+    void *wt = base + R.b;
+    const void *wkrsc = w;
+    const void *dyn = dy;
+    void *dxn = dx;
+    if (G.layout == NNCONV_NCHW) {
+        void *tmp = base + R.d;
+        TRY_HIP(launch_transpose16(w, tmp, G.k, G.cg, G.r * G.s, G.cg, s));
+        wkrsc = tmp;
+        void *dyt = base + R.a;
+        TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, s));
+        dyn = dyt;
+        dxn = base + R.c;
+    }
+    // [g][Kg][R*S*Cg] -> [g][R*S*Cg][Kg]
+    TRY_HIP(launch_transpose16(wkrsc, wt, G.g, G.kg, G.r * G.s * G.cg, G.kg, s));
+    if ((st = dgrad_fast(G, dyn, wt, dxn, alpha, s)) != NNCONV_OK) return st;
+    if (G.layout == NNCONV_NCHW)
+        return hip_status(launch_transpose16(dxn, dx, G.n, G.h * G.w, G.c, G.h * G.w, s));
+    return NNCONV_OK;
+}
+
+NNCONV_API nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, const void *dy,
+                                      void *dw, int32_t dw_dtype, float inv_loss_scale,
+                                      int32_t accumulate, int32_t *overflow_flag, void *ws,
+                                      size_t ws_bytes, void *hip_stream) {
+    Geom G;
+    nnconv_status st = validate(desc, &G);
+    if (st != NNCONV_OK) return st;
+    if (!x || !dy || !dw) return NNCONV_ERR_INVALID_ARG;
+    if (dw_dtype != NNCONV_F32 && dw_dtype != NNCONV_F16 && dw_dtype != NNCONV_BF16)
+        return NNCONV_ERR_INVALID_ARG;
+    if (dw_dtype != NNCONV_F32 && dw_dtype != G.dtype) return NNCONV_ERR_UNSUPPORTED;
+    if (accumulate != 0 && accumulate != 1) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(x, 2) || !aligned(dy, 2) || !aligned(dw, dw_dtype == NNCONV_F32 ? 4 : 2) ||
+        (overflow_flag && !aligned(overflow_flag, 4)))
+        return NNCONV_ERR_MISALIGNED;
+    if ((st = check_ws(G, NNCONV_WGRAD, ws, ws_bytes)) != NNCONV_OK) return st;
+    hipStream_t s = (hipStream_t)hip_stream;
+    clear_stale_error();
+    const int out_code = dw_dtype == NNCONV_F32 ? 2 : (dw_dtype == NNCONV_F16 ? 0 : 1);
+    const int64_t count = G.k * G.r * G.s * G.cg;
+    const int kcrs = G.layout == NNCONV_NCHW;
+    const bool fast = fast_shape(G) && aligned(x, 16) && aligned(dy, 16) && aligned(ws, 16);
+    if (!fast) {
+        const int32_t splits = plan_wgrad_direct_splits(G);
+        float *part = (float *)ws;
+        TRY_HIP(launch_direct_wgrad(G.dtype, direct_params(G, 1.0f), x, dy, part, splits, s));
+        return hip_status(launch_wgrad_reduce(part, splits, count, dw, out_code, inv_loss_scale,
+                                              accumulate, overflow_flag, kcrs, (int32_t)G.cg,
+                                              (int32_t)(G.r * G.s), s));
+    }
+    const Regions R = fast_regions(G, NNCONV_WGRAD);
+    char *base = (char *)ws;
+    const void *xn = x, *dyn = dy;
+    if (G.layout == NNCONV_NCHW) {
+        void *xt = base + R.a, *dyt = base + R.b;
+        TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, s));
+        TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, s));
+        xn = xt;
+        dyn = dyt;
+    }
+    float *part = (float *)(base + R.c);
+    if ((st = wgrad_fast(G, xn, dyn, part, s)) != NNCONV_OK) return st;
+    const WgPlan pl = plan_wgrad_fast(G);
+    return hip_status(launch_wgrad_reduce(part, pl.splits, count, dw, out_code, inv_loss_scale,
+                                          accumulate, overflow_flag, kcrs, (int32_t)G.cg,
+                                          (int32_t)(G.r * G.s), s));
+}
+
+// ---------------------------------------------------------------------------
+// transforms
+// ---------------------------------------------------------------------------
+
+NNCONV_API nnconv_status nnconv_nchw_to_nhwc(const void *src, void *dst, int32_t n, int32_t c,
+                                             int32_t h, int32_t w, int32_t c_pad,
+                                             void *hip_stream) {
+    if (!src || !dst || n < 1 || c < 1 || h < 1 || w < 1 || c_pad < c)
+        return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(src, 2) || !aligned(dst, 2)) return NNCONV_ERR_MISALIGNED;
+    clear_stale_error();
+    return hip_status(launch_transpose16(src, dst, n, c, (int64_t)h * w, c_pad,
+                                         (hipStream_t)hip_stream));
+}
+
+NNCONV_API nnconv_status nnconv_nhwc_to_nchw(const void *src, void *dst, int32_t n, int32_t c,
+                                             int32_t h, int32_t w, void *hip_stream) {
+    if (!src || !dst || n < 1 || c < 1 || h < 1 || w < 1) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(src, 2) || !aligned(dst, 2)) return NNCONV_ERR_MISALIGNED;
+    clear_stale_error();
+    return hip_status(launch_transpose16(src, dst, n, (int64_t)h * w, c, (int64_t)h * w,
+                                         (hipStream_t)hip_stream));
+}
+
+NNCONV_API nnconv_status nnconv_pad_channels(const void *src, void *dst, int64_t rows, int32_t c,
+                                             int32_t c_pad, void *hip_stream) {
+    if (!src || !dst || rows < 1 || c < 1 || c_pad < c) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(src, 2) || !aligned(dst, 2)) return NNCONV_ERR_MISALIGNED;
+    clear_stale_error();
+    return hip_status(launch_pad_channels16(src, dst, rows, c, c_pad, (hipStream_t)hip_stream));
+}
+
+NNCONV_API nnconv_status nnconv_weight_kcrs_to_krsc(const void *src, void *dst, int32_t k,
+                                                    int32_t cg, int32_t r, int32_t s,
+                                                    int32_t cg_pad, void *hip_stream) {
+    if (!src || !dst || k < 1 || cg < 1 || r < 1 || s < 1 || cg_pad < cg)
+        return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(src, 2) || !aligned(dst, 2)) return NNCONV_ERR_MISALIGNED;
+    clear_stale_error();
+    return hip_status(
+        launch_transpose16(src, dst, k, cg, (int64_t)r * s, cg_pad, (hipStream_t)hip_stream));
+}
+
+NNCONV_API nnconv_status nnconv_weight_krsc_to_kcrs(const void *src, void *dst, int32_t k,
+                                                    int32_t cg, int32_t r, int32_t s,
+                                                    void *hip_stream) {
+    if (!src || !dst || k < 1 || cg < 1 || r < 1 || s < 1) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(src, 2) || !aligned(dst, 2)) return NNCONV_ERR_MISALIGNED;
+    clear_stale_error();
+    return hip_status(launch_transpose16(src, dst, k, (int64_t)r * s, cg, (int64_t)r * s,
+                                         (hipStream_t)hip_stream));
+}

@@ -1,0 +1,215 @@
+// direct.hip -- direct convolution kernels (one thread per output element)
+// for geometries the matrix-core kernels do not take: channel counts per
+// group that are not multiples of 8, unaligned pointers, tensors beyond the
+// 2 GiB buffer range, or more than 64 filter taps.  Same semantics as the
+// fast path: fp32 accumulation, round-to-nearest-even output.  Both layouts
+// are handled through element strides.  Also the 16-bit layout transforms.
+#include <type_traits>
+
+#include "launch.hpp"
+
+namespace nnconv {
+
+template <class T>
+__device__ __forceinline__ float ld16(const void *p, int64_t i) {
+    return from16<T>(((const uint16_t *)p)[i]);
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void direct_fwd_kernel(const DirectParams P, const void *x,
+                                                         const void *w, void *y) {
+    const int64_t total = (int64_t)P.n * P.k * P.p * P.q;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= total) return;
+    int64_t f = idx;
+    const int q = (int)(f % P.q); f /= P.q;
+    const int p = (int)(f % P.p); f /= P.p;
+    const int k = (int)(f % P.k); f /= P.k;
+    const int n = (int)f;
+    const int g = k / P.kg;
+    float acc = 0.f;
+    for (int c = 0; c < P.cg; ++c) {
+        const int ci = g * P.cg + c;
+        for (int r = 0; r < P.r; ++r) {
+            const int h = p * P.sh - P.ph + r * P.dh;
+            if (h < 0 || h >= P.h) continue;
+            for (int s = 0; s < P.s; ++s) {
+                const int wv = q * P.sw - P.pw + s * P.dw;
+                if (wv < 0 || wv >= P.w) continue;
+                const float xv = ld16<T>(x, n * P.xs[0] + ci * P.xs[1] + h * P.xs[2] + wv * P.xs[3]);
+                const float fv = ld16<T>(w, k * P.wsd[0] + c * P.wsd[1] + r * P.wsd[2] + s * P.wsd[3]);
+                acc += xv * fv;
+            }
+        }
+    }
+    ((uint16_t *)y)[n * P.ys[0] + k * P.ys[1] + p * P.ys[2] + q * P.ys[3]] =
+        (uint16_t)to16<T>(acc * P.alpha);
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void direct_dgrad_kernel(const DirectParams P, const void *dy,
+                                                           const void *w, void *dx) {
+    const int64_t total = (int64_t)P.n * P.c * P.h * P.w;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= total) return;
+    int64_t f = idx;
+    const int j = (int)(f % P.w); f /= P.w;
+    const int i = (int)(f % P.h); f /= P.h;
+    const int c = (int)(f % P.c); f /= P.c;
+    const int n = (int)f;
+    const int g = c / P.cg;
+    const int cc = c - g * P.cg;
+    float acc = 0.f;
+    for (int kk = 0; kk < P.kg; ++kk) {
+        const int k = g * P.kg + kk;
+        for (int r = 0; r < P.r; ++r) {
+            const int nump = i + P.ph - r * P.dh;
+            if (nump < 0 || nump % P.sh) continue;
+            const int p = nump / P.sh;
+            if (p >= P.p) continue;
+            for (int s = 0; s < P.s; ++s) {
+                const int numq = j + P.pw - s * P.dw;
+                if (numq < 0 || numq % P.sw) continue;
+                const int q = numq / P.sw;
+                if (q >= P.q) continue;
+                const float dv = ld16<T>(dy, n * P.ys[0] + k * P.ys[1] + p * P.ys[2] + q * P.ys[3]);
+                const float fv = ld16<T>(w, k * P.wsd[0] + cc * P.wsd[1] + r * P.wsd[2] + s * P.wsd[3]);
+                acc += dv * fv;
+            }
+        }
+    }
+    ((uint16_t *)dx)[n * P.xs[0] + c * P.xs[1] + i * P.xs[2] + j * P.xs[3]] =
+        (uint16_t)to16<T>(acc * P.alpha);
+}
+
+// ws[split][k][(r*S + s)*Cg + c] = sum over the split's pixels of dy * x
+template <class T>
+__global__ __launch_bounds__(256) void direct_wgrad_kernel(const DirectParams P, const void *x,
+                                                           const void *dy, float *ws,
+                                                           int32_t splits) {
+    const int64_t rscg = (int64_t)P.r * P.s * P.cg;
+    const int64_t count = (int64_t)P.k * rscg;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int split = blockIdx.y;
+    if (idx >= count) return;
+    const int k = (int)(idx / rscg);
+    const int64_t jj = idx - (int64_t)k * rscg;
+    const int tap = (int)(jj / P.cg);
+    const int c = (int)(jj - (int64_t)tap * P.cg);
+    const int r = tap / P.s, s = tap - (tap / P.s) * P.s;
+    const int ci = (k / P.kg) * P.cg + c;
+    const int64_t npq = (int64_t)P.n * P.p * P.q;
+    const int64_t per = (npq + splits - 1) / splits;
+    const int64_t b = split * per;
+    const int64_t e = b + per < npq ? b + per : npq;
+    float acc = 0.f;
+    for (int64_t pix = b; pix < e; ++pix) {
+        const int n = (int)(pix / ((int64_t)P.p * P.q));
+        const int rm = (int)(pix - (int64_t)n * P.p * P.q);
+        const int p = rm / P.q, q = rm - (rm / P.q) * P.q;
+        const int h = p * P.sh - P.ph + r * P.dh;
+        const int wv = q * P.sw - P.pw + s * P.dw;
+        if (h < 0 || h >= P.h || wv < 0 || wv >= P.w) continue;
+        const float xv = ld16<T>(x, n * P.xs[0] + ci * P.xs[1] + h * P.xs[2] + wv * P.xs[3]);
+        const float dv = ld16<T>(dy, n * P.ys[0] + k * P.ys[1] + p * P.ys[2] + q * P.ys[3]);
+        acc += dv * xv;
+    }
+    ws[(int64_t)split * count + idx] = acc;
+}
+
+hipError_t launch_direct_fwd(int dtype, const DirectParams &p, const void *x, const void *w,
+                             void *y, hipStream_t st) {
+    const int64_t total = (int64_t)p.n * p.k * p.p * p.q;
+    const dim3 grid((uint32_t)((total + 255) / 256));
+    if (dtype == Half::id)
+        hipLaunchKernelGGL(direct_fwd_kernel<Half>, grid, dim3(256), 0, st, p, x, w, y);
+    else
+        hipLaunchKernelGGL(direct_fwd_kernel<BFloat>, grid, dim3(256), 0, st, p, x, w, y);
+    return hipGetLastError();
+}
+
+hipError_t launch_direct_dgrad(int dtype, const DirectParams &p, const void *dy, const void *w,
+                               void *dx, hipStream_t st) {
+    const int64_t total = (int64_t)p.n * p.c * p.h * p.w;
+    const dim3 grid((uint32_t)((total + 255) / 256));
+    if (dtype == Half::id)
+        hipLaunchKernelGGL(direct_dgrad_kernel<Half>, grid, dim3(256), 0, st, p, dy, w, dx);
+    else
+        hipLaunchKernelGGL(direct_dgrad_kernel<BFloat>, grid, dim3(256), 0, st, p, dy, w, dx);
+    return hipGetLastError();
+}
+
+hipError_t launch_direct_wgrad(int dtype, const DirectParams &p, const void *x, const void *dy,
+                               float *ws, int32_t splits, hipStream_t st) {
+    const int64_t count = (int64_t)p.k * p.r * p.s * p.cg;
+    const dim3 grid((uint32_t)((count + 255) / 256), (uint32_t)splits);
+    if (dtype == Half::id)
+        hipLaunchKernelGGL(direct_wgrad_kernel<Half>, grid, dim3(256), 0, st, p, x, dy, ws, splits);
+    else
+        hipLaunchKernelGGL(direct_wgrad_kernel<BFloat>, grid, dim3(256), 0, st, p, x, dy, ws,
+                           splits);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// 16-bit transforms
+// ---------------------------------------------------------------------------
+
+// dst[b][cc][rr] = rr < rows ? src[b][rr][cc] : 0, through a 64x64 LDS tile
+// (reads coalesced along cc, writes coalesced along rr).
+__global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__restrict__ src,
+                                                          uint16_t *__restrict__ dst, int64_t rows,
+                                                          int64_t cols, int64_t dst_ld,
+                                                          int64_t tiles_c, int64_t tiles_r) {
+    __shared__ uint16_t tile[64][65];
+    const int64_t t = blockIdx.x;
+    const int64_t b = t / (tiles_c * tiles_r);
+    const int64_t rem = t - b * tiles_c * tiles_r;
+    const int64_t tr = rem / tiles_c, tc = rem - (rem / tiles_c) * tiles_c;
+    const int64_t r0 = tr * 64, c0 = tc * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const uint16_t *s = src + b * rows * cols;
+    for (int i = ty; i < 64; i += 4) {
+        const int64_t rr = r0 + i, cc = c0 + tx;
+        tile[i][tx] = (rr < rows && cc < cols) ? s[rr * cols + cc] : (uint16_t)0;
+    }
+    __syncthreads();
+    uint16_t *d = dst + b * cols * dst_ld;
+    for (int i = ty; i < 64; i += 4) {
+        const int64_t cc = c0 + i, rr = r0 + tx;
+        if (cc < cols && rr < dst_ld) d[cc * dst_ld + rr] = tile[tx][i];
+    }
+}
+
+hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
+                              int64_t cols, int64_t dst_ld, hipStream_t st) {
+    const int64_t tiles_c = (cols + 63) / 64, tiles_r = (dst_ld + 63) / 64;
+    const int64_t nb = batch * tiles_c * tiles_r;
+    if (nb <= 0) return hipSuccess;
+    hipLaunchKernelGGL(transpose16_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
+                       (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
+                       tiles_r);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void pad_channels16_kernel(const uint16_t *__restrict__ src,
+                                                             uint16_t *__restrict__ dst,
+                                                             int64_t total, int32_t c,
+                                                             int32_t c_pad) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= total) return;
+    const int64_t row = i / c_pad;
+    const int ch = (int)(i - row * c_pad);
+    dst[i] = ch < c ? src[row * c + ch] : (uint16_t)0;
+}
+
+hipError_t launch_pad_channels16(const void *src, void *dst, int64_t rows, int32_t c,
+                                 int32_t c_pad, hipStream_t st) {
+    const int64_t total = rows * c_pad;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(pad_channels16_kernel, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0,
+                       st, (const uint16_t *)src, (uint16_t *)dst, total, c, c_pad);
+    return hipGetLastError();
+}
+
+}  // namespace nnconv

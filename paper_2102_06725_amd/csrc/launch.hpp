@@ -1,0 +1,120 @@
+// launch.hpp -- host-side interface between the C-ABI shim and the kernel
+// translation units.  Plain structs only; every launcher queues work on the
+// given stream and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace nnconv {
+
+constexpr int MAX_TAPS = 64;
+
+// Filter taps visited by one implicit-GEMM launch.  Tap t moves the A-image
+// read position by (dh[t], dw[t]) and starts at element boff[t] of a B row.
+struct TapTable {
+    int32_t n;
+    int32_t dh[MAX_TAPS];
+    int32_t dw[MAX_TAPS];
+    int32_t boff[MAX_TAPS];
+};
+
+// One implicit GEMM  out[row, col] = alpha * sum_{tap, ch} A(row, tap, ch) * B[col, tap, ch]
+// with channel-last operands, used for the forward pass (A = x, B = w) and
+// for one stride phase of the backward-data pass (A = dy, B = w transposed
+// to [R][S][Cg][Kg] per group).
+//
+// Row m decodes to (image n, i, j) with i < mi, j < mj.  A is read at pixel
+// (i*ai_mul + ai_add + dh[t], j*aj_mul + aj_add + dw[t]) of image n (zero
+// outside a_h x a_w), channels g*a_cg_ofs + ch.  B row `col` of group g
+// starts at element g*b_g_ofs + col*b_ld.  The result goes to pixel
+// (i*oi_mul + oi_add, j*oj_mul + oj_add) of an o_h x o_w image with o_c
+// channels, channel g*o_cg_ofs + col.
+struct TNParams {
+    const void *a;
+    uint32_t a_bytes;
+    const void *b;
+    uint32_t b_bytes;
+    void *out;
+    int32_t M;
+    int32_t mi, mj;
+    FastDiv div_mj, div_mi;
+    int32_t a_h, a_w, a_c, a_cg_ofs;
+    int32_t ai_mul, ai_add, aj_mul, aj_add;
+    int32_t cr;            // reduction channels per tap (multiple of 8)
+    FastDiv div_crv;       // division by cr / 8
+    int32_t k_iters;       // ceil(taps * cr / 64)
+    int32_t ncols;         // output columns per group (multiple of 8)
+    int32_t b_ld, b_g_ofs;
+    int32_t o_h, o_w, o_c, o_cg_ofs;
+    int32_t oi_mul, oi_add, oj_mul, oj_add;
+    float alpha;
+    int32_t groups;
+    int32_t tiles_m, tiles_n;  // per group; filled by the launcher
+    TapTable taps;
+};
+
+enum TNConfig { TN_128x128 = 0, TN_256x64 = 1, TN_256x128 = 2 };
+
+hipError_t launch_igemm_tn(int dtype, TNConfig cfg, TNParams &p, hipStream_t st);
+
+// Backward-weight split-K partial sums:
+//   ws[split][k][j] = sum over pixels of this split of dy[pix, k] * xcol[pix, j]
+// with j = (r*S + s)*Cg + c (the [K][R][S][Cg] order) and channel-last x, dy.
+struct WGParams {
+    const void *x;
+    uint32_t x_bytes;
+    const void *dy;
+    uint32_t dy_bytes;
+    float *ws;
+    int32_t h, w, c, k;         // x height/width/channels, dy channels
+    int32_t cg, kg;
+    int32_t p, q, npq;
+    FastDiv div_q, div_pq, div_cg, div_s;
+    int32_t sh, sw, ph, pw, dh, dw;
+    int32_t rscg;
+    int32_t groups, splits, pix_per_split;
+    int32_t tiles_m, tiles_n;   // filled by the launcher
+};
+
+enum WGConfig { WG_128x128 = 0, WG_64x128 = 1 };
+
+hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);
+
+// dw[e'] = (accumulate ? dw[e'] : 0) + inv_scale * sum_{s < splits} ws[s][e]
+// over e < count = K * R*S*Cg; e' = e for [K][R][S][Cg] output, or the
+// matching [K][Cg][R][S] index when kcrs != 0.  Stores 1 into *flag when a
+// final value is not finite.
+hipError_t launch_wgrad_reduce(const float *ws, int32_t splits, int64_t count, void *dw,
+                               int out_dtype, float inv_scale, int accumulate, int32_t *flag,
+                               int kcrs, int32_t cg, int32_t rs, hipStream_t st);
+
+// Direct (one thread per output) kernels for any valid geometry and either
+// layout; element offsets are given by strides.
+struct DirectParams {
+    int32_t n, c, h, w, k, r, s, p, q;
+    int32_t sh, sw, ph, pw, dh, dw, groups, cg, kg;
+    int64_t xs[4];   // x strides for (n, c, h, w)
+    int64_t ys[4];   // y / dy strides for (n, k, p, q)
+    int64_t wsd[4];  // w strides for (k, c, r, s)
+    float alpha;
+};
+
+hipError_t launch_direct_fwd(int dtype, const DirectParams &p, const void *x, const void *w,
+                             void *y, hipStream_t st);
+hipError_t launch_direct_dgrad(int dtype, const DirectParams &p, const void *dy, const void *w,
+                               void *dx, hipStream_t st);
+// Raw sums into ws[split][k][(r*S+s)*Cg + c], pixels split into `splits` ranges.
+hipError_t launch_direct_wgrad(int dtype, const DirectParams &p, const void *x, const void *dy,
+                               float *ws, int32_t splits, hipStream_t st);
+
+// dst[b][cc][rr] = rr < rows ? src[b][rr][cc] : 0   for rr < dst_ld, cc < cols
+hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
+                              int64_t cols, int64_t dst_ld, hipStream_t st);
+// dst[row][ch] = ch < c ? src[row][ch] : 0   for ch < c_pad
+hipError_t launch_pad_channels16(const void *src, void *dst, int64_t rows, int32_t c,
+                                 int32_t c_pad, hipStream_t st);
+
+}  // namespace nnconv

@@ -1,0 +1,135 @@
+"""C-ABI of libnnconv on the host: exported symbols, argument validation and
+shape arithmetic.  Every call here fails validation (or only computes sizes)
+before anything is queued, so no GPU is needed and no kernel runs."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2102_06725_amd import nnconv as nc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "nnconv.h")).read()
+    return sorted(set(re.findall(r"\b(nnconv_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(nnlib):
+    declared = header_functions()
+    assert len(declared) >= 12
+    for name in declared:
+        assert hasattr(nnlib, name), name
+    assert set(declared) == set(nc.EXPORTS)
+
+
+def test_version_and_strings(nnlib):
+    assert nc.nnconv_version() == 1
+    for s in range(6):
+        assert nc.status_string(s)
+
+
+def good_desc(**kw):
+    base = dict(n=2, c=16, h=16, w=16, k=16, r=3, s=3, stride=(1, 1), pad=(1, 1))
+    base.update(kw)
+    return nc.make_desc(**base)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(n=0), dict(c=0), dict(h=-1), dict(k=0), dict(r=0),
+    dict(stride=(0, 1)), dict(dil=(1, 0)), dict(pad=(-1, 0)),
+    dict(groups=3), dict(groups=0), dict(c=16, k=12, groups=8),
+    dict(h=2, w=2, r=5, s=5, pad=(0, 0)),        # empty output
+    dict(layout=7), dict(dtype=9),
+])
+def test_invalid_descriptors(nnlib, kw):
+    d = good_desc(**kw)
+    st, _, _ = nc.nnconv_output_dims(d)
+    assert st == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_fwd(d, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_dgrad(d, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_wgrad(d, FAKE, FAKE, FAKE, nc.NNCONV_F32, 1.0, 0, None, FAKE, 1 << 30,
+                           None) == nc.NNCONV_ERR_INVALID_ARG
+
+
+def test_fp32_operands_unsupported(nnlib):
+    d = good_desc(dtype=nc.NNCONV_F32)
+    assert nc.nnconv_fwd(d, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None) == nc.NNCONV_ERR_UNSUPPORTED
+
+
+def test_null_and_misaligned_pointers(nnlib):
+    d = good_desc(layout=nc.NNCONV_NHWC)
+    assert nc.nnconv_fwd(d, None, FAKE, FAKE, 1.0, FAKE, 1 << 30, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_dgrad(d, FAKE, FAKE, None, 1.0, FAKE, 1 << 30, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_wgrad(d, FAKE, None, FAKE, nc.NNCONV_F32, 1.0, 0, None, FAKE, 1 << 30,
+                           None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_fwd(d, FAKE + 1, FAKE, FAKE, 1.0, FAKE, 1 << 30, None) == nc.NNCONV_ERR_MISALIGNED
+    assert nc.nnconv_wgrad(d, FAKE, FAKE, FAKE + 2, nc.NNCONV_F32, 1.0, 0, None, FAKE, 1 << 30,
+                           None) == nc.NNCONV_ERR_MISALIGNED
+
+
+def test_bad_wgrad_options(nnlib):
+    d = good_desc(layout=nc.NNCONV_NHWC)
+    assert nc.nnconv_wgrad(d, FAKE, FAKE, FAKE, nc.NNCONV_BF16, 1.0, 0, None, FAKE, 1 << 30,
+                           None) == nc.NNCONV_ERR_UNSUPPORTED
+    assert nc.nnconv_wgrad(d, FAKE, FAKE, FAKE, 5, 1.0, 0, None, FAKE, 1 << 30,
+                           None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_wgrad(d, FAKE, FAKE, FAKE, nc.NNCONV_F32, 1.0, 2, None, FAKE, 1 << 30,
+                           None) == nc.NNCONV_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("layout", [nc.NNCONV_NCHW, nc.NNCONV_NHWC])
+def test_workspace_too_small(nnlib, layout):
+    d = good_desc(layout=layout)
+    for pass_, call in ((nc.NNCONV_FWD, lambda ws, nb: nc.nnconv_fwd(d, FAKE, FAKE, FAKE, 1.0, ws, nb, None)),
+                        (nc.NNCONV_DGRAD, lambda ws, nb: nc.nnconv_dgrad(d, FAKE, FAKE, FAKE, 1.0, ws, nb, None)),
+                        (nc.NNCONV_WGRAD, lambda ws, nb: nc.nnconv_wgrad(d, FAKE, FAKE, FAKE, nc.NNCONV_F32,
+                                                                         1.0, 0, None, ws, nb, None))):
+        st, need = nc.nnconv_workspace_size(d, pass_)
+        assert st == nc.NNCONV_OK
+        if need == 0:
+            continue
+        assert call(FAKE, need - 1) == nc.NNCONV_ERR_WORKSPACE
+        assert call(None, need) == nc.NNCONV_ERR_INVALID_ARG
+
+
+def test_workspace_sizes_are_deterministic_and_cover_partials(nnlib):
+    d = good_desc(n=64, c=64, h=56, w=56, k=64, layout=nc.NNCONV_NHWC)
+    st, f = nc.nnconv_workspace_size(d, nc.NNCONV_FWD)
+    assert st == 0 and f == 0                      # channel-last forward needs no scratch
+    st, w1 = nc.nnconv_workspace_size(d, nc.NNCONV_WGRAD)
+    st, w2 = nc.nnconv_workspace_size(d, nc.NNCONV_WGRAD)
+    assert w1 == w2 and w1 >= 64 * 9 * 64 * 4    # at least one fp32 partial of dw
+    st, dg = nc.nnconv_workspace_size(d, nc.NNCONV_DGRAD)
+    assert dg >= 64 * 9 * 64 * 2                 # transposed weights
+    assert nc.nnconv_workspace_size(d, 7)[0] == nc.NNCONV_ERR_INVALID_ARG
+
+
+def test_output_dims_match_oracle(nnlib, oracle_lib):
+    import oracle.oracle as orc
+    for h in range(1, 12):
+        for r in (1, 2, 3, 5, 7):
+            for st in (1, 2, 3):
+                for pd in (0, 1, 3):
+                    for dl in (1, 2):
+                        d = nc.make_desc(1, 8, h, h + 1, 8, r, r, (st, st), (pd, pd), (dl, dl))
+                        s, p, q = nc.nnconv_output_dims(d)
+                        try:
+                            cv = orc.Conv(1, 8, h, h + 1, 8, r, r, (st, st), (pd, pd), (dl, dl), 1,
+                                          lib=oracle_lib)
+                        except ValueError:
+                            assert s == nc.NNCONV_ERR_INVALID_ARG
+                            continue
+                        assert s == 0 and (p, q) == (cv.p, cv.q)
+
+
+def test_transform_validation(nnlib):
+    assert nc.nnconv_nchw_to_nhwc(FAKE, FAKE, 1, 3, 4, 4, 2, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_nchw_to_nhwc(None, FAKE, 1, 3, 4, 4, 8, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_pad_channels(FAKE + 1, FAKE, 10, 3, 8, None) == nc.NNCONV_ERR_MISALIGNED
+    assert nc.nnconv_weight_kcrs_to_krsc(FAKE, FAKE, 4, 3, 3, 3, 2, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_weight_krsc_to_kcrs(FAKE, FAKE, 0, 3, 3, 3, None) == nc.NNCONV_ERR_INVALID_ARG
+    assert nc.nnconv_nhwc_to_nchw(FAKE, None, 1, 3, 4, 4, None) == nc.NNCONV_ERR_INVALID_ARG

@@ -1,0 +1,348 @@
+"""Benchmark: mixed-precision convolution fwd + dgrad + wgrad throughput on
+ResNet-50 shapes, one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--workload sweep]
+
+One step = one pass of the whole path over one batch: for every one of
+ResNet-50 v1.5's 53 convolution layers at batch 256 (channel-last fp16,
+loss scale 1024): the stem's 3->8 channel padding, forward, backward-data
+(not for the stem: no gradient to the image), backward-weight split-K with
+its reduction / loss-scale epilogue into fp32 dw, and the shared overflow
+flag.  Every layer has its own activation, weight and gradient buffers;
+inputs are seeded synthetic draws already resident in HBM.  Prints one
+JSON line.
+
+value = sum of algorithmic FLOPs (2*N*K*P*Q*Cg*R*S per pass, stem with its
+3 logical channels) / wall time of the timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_F16_TFLOPS = 2516.6     # 256 CU x 4096 flop/clk x 2.4 GHz, dense fp16/bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+METRIC = "conv fwd+dgrad+wgrad TFLOP/s on ResNet-50 shapes; % of fp16 MFMA peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "cfg2", "cfg3", "cfg4"])
+    ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
+    ap.add_argument("--batch", type=int, default=0, help="override the batch size")
+    ap.add_argument("--cpu-seconds", type=float, default=30.0,
+                    help="upper bound on the oracle CPU-baseline sample (0 disables it)")
+    ap.add_argument("--no-events", action="store_true",
+                    help="skip the per-call HIP events inside the timed steps")
+    ap.add_argument("--layers", default="",
+                    help="comma-separated layer names: run only these layers of the workload "
+                         "(for profiling one shape; the reported value then covers only them)")
+    ap.add_argument("--per-layer", default="",
+                    help="write a per-layer / per-pass roofline table to this file")
+    return ap.parse_args()
+
+
+def layers_for(args):
+    from paper_2102_06725_amd import inputs as I
+    if args.workload == "sweep":
+        wl = I.workload(5, args.dtype, batch=args.batch or None)
+        expanded = []
+        for l, c in I.resnet50_layers(wl.layers[0].n):
+            expanded += [l] * c
+        if args.layers:
+            keep = set(args.layers.split(","))
+            expanded = [l for l in expanded if l.name in keep]
+        return wl, expanded
+    cfg = {"cfg2": 2, "cfg3": 3, "cfg4": 4}[args.workload]
+    wl = I.workload(cfg, args.dtype, batch=args.batch or None)
+    return wl, list(wl.layers)
+
+
+class LayerBuffers:
+    def __init__(self, L, wl, seed, dev, torch, nc):
+        self.L = L
+        self.torch = torch
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed)
+        tdt = torch.float16 if wl.dtype == "f16" else torch.bfloat16
+        cl = L.c_alg
+        # x: ReLU-like |N(0,1)| activations (the stem: N(0,1) pixels), channel-last
+        x = torch.randn((L.n, L.h, L.w, cl), generator=g, device=dev, dtype=torch.float32)
+        if wl.x_kind == "absnormal":
+            x.abs_()
+        self.x_raw = x.to(tdt)
+        if cl != L.c:
+            self.x = torch.empty((L.n, L.h, L.w, L.c), device=dev, dtype=tdt)
+        else:
+            self.x = self.x_raw
+        std = math.sqrt(2.0 / (cl * L.r * L.s))
+        w = torch.zeros((L.k, L.r, L.s, L.c), device=dev, dtype=torch.float32)
+        w[..., :cl] = torch.randn((L.k, L.r, L.s, cl), generator=g, device=dev) * std
+        self.w = w.to(tdt)
+        dy = torch.randn((L.n, L.p, L.q, L.k), generator=g, device=dev) * (wl.loss_scale * wl.dy_std)
+        self.dy = dy.to(tdt)
+        del x, w, dy
+        self.y = torch.empty((L.n, L.p, L.q, L.k), device=dev, dtype=tdt)
+        self.dx = torch.empty((L.n, L.h, L.w, L.c), device=dev, dtype=tdt) if L.dgrad else None
+        self.dw = torch.empty((L.k, L.r, L.s, L.c), device=dev, dtype=torch.float32)
+        self.desc = nc.make_desc(L.n, L.c, L.h, L.w, L.k, L.r, L.s, (L.stride, L.stride),
+                                 (L.pad, L.pad), (L.dil, L.dil), L.groups, nc.NNCONV_NHWC,
+                                 nc.NNCONV_F16 if wl.dtype == "f16" else nc.NNCONV_BF16)
+        self.ws_need = {}
+        for p in (nc.NNCONV_FWD, nc.NNCONV_DGRAD, nc.NNCONV_WGRAD):
+            st, nb = nc.nnconv_workspace_size(self.desc, p)
+            nc.check(st, "workspace_size")
+            self.ws_need[p] = nb
+
+
+def compulsory_bytes(L, pass_):
+    """Bytes a pass must move at least once: its operands and its output
+    (2-byte elements, fp32 dw).  For strided 1x1 layers only the sampled
+    pixels of x are read."""
+    e = 2
+    x_full = L.n * L.h * L.w * L.c * e
+    if L.r == 1 and L.s == 1 and L.pad == 0:
+        x_read = L.n * L.p * L.q * L.c * e
+    else:
+        x_read = x_full
+    y = L.n * L.p * L.q * L.k * e
+    w = L.k * L.r * L.s * (L.c // L.groups) * e
+    if pass_ == "fwd":
+        return x_read + w + y
+    if pass_ == "dgrad":
+        return y + w + x_full
+    return x_read + y + 2 * w
+
+
+def roofline_us(L, pass_):
+    t_mfma = L.flops(executed=True) / (PEAK_F16_TFLOPS * 1e12)
+    t_hbm = compulsory_bytes(L, pass_) / (PEAK_HBM_GBS * 1e9)
+    return max(t_mfma, t_hbm) * 1e6, ("mfma" if t_mfma >= t_hbm else "hbm")
+
+
+def write_per_layer(path, layers, ev_steps, steps):
+    rows = []
+    for i, L in enumerate(layers):
+        for pi, pname in enumerate(("fwd", "dgrad", "wgrad")):
+            if pname == "dgrad" and not L.dgrad:
+                continue
+            us = sum(ev[i][pi].elapsed_time(ev[i][pi + 1]) for ev in ev_steps) / steps * 1e3
+            bound_us, bound = roofline_us(L, pname)
+            rows.append((i, L.name, pname, us, L.flops() / (us * 1e-6) / 1e12, bound,
+                         bound_us, 100.0 * bound_us / us))
+    with open(path, "w") as f:
+        f.write("%-3s %-10s %-6s %9s %8s %5s %9s %7s\n" % ("i", "layer", "pass", "us", "TFLOP/s",
+                                                          "bound", "roof_us", "%roof"))
+        for r in rows:
+            f.write("%-3d %-10s %-6s %9.1f %8.1f %5s %9.1f %7.1f\n" % r)
+        tot = sum(r[3] for r in rows)
+        roof = sum(r[6] for r in rows)
+        f.write("total %.1f us, roofline %.1f us (%.1f%%)\n" % (tot, roof, 100 * roof / tot))
+
+
+def cpu_baseline(args, wl):
+    """The fp64 oracle as it stands, timed on this host's cores over a bounded
+    sample: every distinct layer shape of the workload at batch 8, all its
+    passes, stopping once the time bound is reached."""
+    import numpy as np
+    import oracle.oracle as orc
+    from paper_2102_06725_amd import inputs as I
+    orc.build(force=False)
+    cores = len(os.sched_getaffinity(0))
+    orc.set_threads(cores)
+    seen = []
+    for L in wl.layers:
+        if L not in seen:
+            seen.append(L)
+    flops = 0
+    t_total = 0.0
+    done = 0
+    passes_done = 0
+    for li, L in enumerate(seen):
+        Ls = L.with_batch(8)
+        cl = Ls.c_alg
+        cv = orc.Conv(Ls.n, cl, Ls.h, Ls.w, Ls.k, Ls.r, Ls.s, (Ls.stride,) * 2, (Ls.pad,) * 2,
+                      (Ls.dil,) * 2, Ls.groups)
+        rng = np.random.default_rng(7000 + li)
+        x = np.abs(rng.standard_normal(cv.x_shape))
+        w = rng.standard_normal(cv.w_shape) * math.sqrt(2.0 / (cl * Ls.r * Ls.s))
+        dy = rng.standard_normal(cv.y_shape) * 1.024
+        t0 = time.perf_counter()
+        cv.fwd(x, w)
+        n_pass = 1
+        if Ls.dgrad:
+            cv.dgrad(dy, w)
+            n_pass += 1
+        cv.wgrad(x, dy, 1.0 / 1024)
+        n_pass += 1
+        t_total += time.perf_counter() - t0
+        flops += Ls.flops() * n_pass
+        passes_done += n_pass
+        done += 1
+        if t_total > args.cpu_seconds:
+            break
+    return {
+        "value": flops / t_total / 1e12,
+        "unit": "TFLOP/s",
+        "cores": orc.get_threads(),
+        "kind": "oracle",
+        "sample": "fp64 direct-loop oracle, %d of %d distinct layer shapes at batch 8 "
+                  "(%d passes, %.1f GFLOP) in %.1f s" % (done, len(seen), passes_done,
+                                                        flops / 1e9, t_total),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only (this build has no multi-GPU path); "
+              "got --gpus %d" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2102_06725_amd import nnconv as nc
+
+    nc.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+
+    wl, layers = layers_for(args)
+    bufs = [LayerBuffers(L, wl, 1_000_000 * 5 + 1000 * i + 1, dev, torch, nc)
+            for i, L in enumerate(layers)]
+    ws_bytes = max(max(b.ws_need.values()) for b in bufs)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    inv_s = 1.0 / wl.loss_scale
+    torch.cuda.synchronize()
+
+    def one_step(ev):
+        flag.zero_()
+        for i, b in enumerate(bufs):
+            L = b.L
+            if b.x is not b.x_raw:
+                nc.check(nc.nnconv_pad_channels(b.x_raw.data_ptr(), b.x.data_ptr(),
+                                                L.n * L.h * L.w, L.c_alg, L.c, sptr), "pad")
+            if ev is not None:
+                ev[i][0].record(stream)
+            nc.check(nc.nnconv_fwd(b.desc, b.x.data_ptr(), b.w.data_ptr(), b.y.data_ptr(), 1.0,
+                                   ws.data_ptr(), ws_bytes, sptr), "fwd")
+            if ev is not None:
+                ev[i][1].record(stream)
+            if L.dgrad:
+                nc.check(nc.nnconv_dgrad(b.desc, b.dy.data_ptr(), b.w.data_ptr(), b.dx.data_ptr(),
+                                         1.0, ws.data_ptr(), ws_bytes, sptr), "dgrad")
+            if ev is not None:
+                ev[i][2].record(stream)
+            nc.check(nc.nnconv_wgrad(b.desc, b.x.data_ptr(), b.dy.data_ptr(), b.dw.data_ptr(),
+                                     nc.NNCONV_F32, inv_s, 0, flag.data_ptr(), ws.data_ptr(),
+                                     ws_bytes, sptr), "wgrad")
+            if ev is not None:
+                ev[i][3].record(stream)
+
+    for _ in range(args.warmup):
+        one_step(None)
+    torch.cuda.synchronize()
+
+    use_ev = not args.no_events
+    ev_steps = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in bufs] if use_ev else None
+        one_step(ev)
+        if use_ev:
+            ev_steps.append(ev)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    elapsed = t1 - t0
+    if int(flag.item()) != 0:
+        print("warning: overflow flag set during the benchmark", file=sys.stderr)
+
+    step_flops = sum(L.flops() * (3 if L.dgrad else 2) for L in layers)
+    value = step_flops * args.steps / elapsed / 1e12
+
+    # per-pass time from the events inside the timed steps
+    pass_ms = {"fwd": 0.0, "dgrad": 0.0, "wgrad": 0.0}
+    pass_flops = {"fwd": 0, "dgrad": 0, "wgrad": 0}
+    pass_launch_units = {"fwd": 0, "dgrad": 0, "wgrad": 0}
+    if use_ev:
+        for ev in ev_steps:
+            for i, b in enumerate(bufs):
+                pass_ms["fwd"] += ev[i][0].elapsed_time(ev[i][1])
+                pass_ms["dgrad"] += ev[i][1].elapsed_time(ev[i][2])
+                pass_ms["wgrad"] += ev[i][2].elapsed_time(ev[i][3])
+        for L in layers:
+            pass_flops["fwd"] += L.flops() * args.steps
+            pass_launch_units["fwd"] += args.steps
+            pass_flops["wgrad"] += L.flops() * args.steps
+            pass_launch_units["wgrad"] += args.steps
+            if L.dgrad:
+                pass_flops["dgrad"] += L.flops() * args.steps
+                pass_launch_units["dgrad"] += args.steps
+    roofline = None
+    per_pass = {}
+    if use_ev:
+        for k in pass_ms:
+            if pass_ms[k] > 0:
+                per_pass[k] = {"ms_per_step": pass_ms[k] / args.steps,
+                               "tflops": pass_flops[k] / (pass_ms[k] * 1e-3) / 1e12}
+        # The forward pass is one kernel launch per layer (the implicit-GEMM
+        # forward kernel), so its per-call event time is that kernel's launch
+        # duration.
+        fwd_avg_ms = pass_ms["fwd"] / pass_launch_units["fwd"]
+        fwd_avg_flops = pass_flops["fwd"] / pass_launch_units["fwd"]
+        ach = fwd_avg_flops / (fwd_avg_ms * 1e-3) / 1e12
+        roofline = {"kernel": "igemm_tn_kernel (forward launches)", "bound": "mfma",
+                    "achieved": ach, "peak": PEAK_F16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": ach / PEAK_F16_TFLOPS, "traffic": None,
+                    "avg_launch_us": fwd_avg_ms * 1e3,
+                    "avg_flops_per_launch": fwd_avg_flops}
+
+    if args.per_layer and use_ev:
+        write_per_layer(args.per_layer, layers, ev_steps, args.steps)
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(args, wl)
+
+    L0 = layers[0]
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic (seeded; no dataset)",
+        "config": {"workload": wl.name + ", channel-last %s, fwd+dgrad+wgrad (stem fwd+wgrad), "
+                               "loss scale %g, fp32 dw" % (args.dtype, wl.loss_scale),
+                   "batch": L0.n, "layers": len(layers),
+                   "layer_passes": sum(3 if L.dgrad else 2 for L in layers),
+                   "tflop_per_step": step_flops / 1e12},
+        "pct_of_peak": 100.0 * value / PEAK_F16_TFLOPS,
+        "per_pass": per_pass,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -205,6 +205,12 @@ TNParams tn_base() {
 
 TNConfig pick_tn(int64_t ncols) { return ncols <= 64 ? TN_256x64 : TN_128x128; }
 
+V3Config pick_v3(int64_t ncols) {
+    if (ncols <= 64) return V3_256x64;
+    if (ncols <= 128) return V3_256x128;
+    return V3_256x256;
+}
+
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
                        hipStream_t st) {
     TNParams p = tn_base();
@@ -241,7 +247,9 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
         }
     p.taps.n = t;
     p.k_iters = (int32_t)((int64_t(t) * G.cg + 63) / 64);
-    return hip_status(launch_igemm_tn(G.dtype, pick_tn(G.kg), p, st));
+    if (G.cg % 64 == 0)
+        return hip_status(launch_igemm_v3(G.dtype, pick_v3(G.kg), p, G.ph > 0 || G.pw > 0, st));
+    return hip_status(launch_igemm_dma(G.dtype, pick_tn(G.kg), p, st));
 }
 
 // Backward-data as sigma_h * sigma_w independent implicit GEMMs, one per
@@ -294,7 +302,11 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             }
             p.taps.n = t;
             p.k_iters = (int32_t)((int64_t(t) * G.kg + 63) / 64);
-            TRY_HIP(launch_igemm_tn(G.dtype, pick_tn(G.cg), p, st));
+            const bool pad = !(G.r == 1 && G.s == 1 && G.ph == 0 && G.pw == 0);
+            if (G.kg % 64 == 0)
+                TRY_HIP(launch_igemm_v3(G.dtype, pick_v3(G.cg), p, pad, st));
+            else
+                TRY_HIP(launch_igemm_dma(G.dtype, pick_tn(G.cg), p, st));
         }
     }
     return NNCONV_OK;

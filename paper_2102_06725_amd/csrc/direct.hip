@@ -203,12 +203,41 @@ __global__ __launch_bounds__(256) void pad_channels16_kernel(const uint16_t *__r
     dst[i] = ch < c ? src[row * c + ch] : (uint16_t)0;
 }
 
+// c_pad a multiple of 8 and dst 16-byte aligned: one thread builds one
+// 8-channel (16-byte) chunk of the output and stores it whole.
+__global__ __launch_bounds__(256) void pad_channels16_vec_kernel(const uint16_t *__restrict__ src,
+                                                                 u32x4 *__restrict__ dst,
+                                                                 int64_t chunks, int32_t c,
+                                                                 int32_t chunks_per_row) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= chunks) return;
+    const int64_t row = i / chunks_per_row;
+    const int ch0 = (int)(i - row * chunks_per_row) * 8;
+    const uint16_t *s = src + row * c;
+    uint32_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int a = ch0 + 2 * u, b = a + 1;
+        const uint32_t lo = a < c ? s[a] : 0u;
+        const uint32_t hi = b < c ? s[b] : 0u;
+        v[u] = lo | (hi << 16);
+    }
+    dst[i] = u32x4{v[0], v[1], v[2], v[3]};
+}
+
 hipError_t launch_pad_channels16(const void *src, void *dst, int64_t rows, int32_t c,
                                  int32_t c_pad, hipStream_t st) {
     const int64_t total = rows * c_pad;
     if (total <= 0) return hipSuccess;
-    hipLaunchKernelGGL(pad_channels16_kernel, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0,
-                       st, (const uint16_t *)src, (uint16_t *)dst, total, c, c_pad);
+    if (c_pad % 8 == 0 && ((uintptr_t)dst % 16) == 0) {
+        const int64_t chunks = total / 8;
+        hipLaunchKernelGGL(pad_channels16_vec_kernel, dim3((uint32_t)((chunks + 255) / 256)),
+                           dim3(256), 0, st, (const uint16_t *)src, (u32x4 *)dst, chunks, c,
+                           c_pad / 8);
+    } else {
+        hipLaunchKernelGGL(pad_channels16_kernel, dim3((uint32_t)((total + 255) / 256)), dim3(256),
+                           0, st, (const uint16_t *)src, (uint16_t *)dst, total, c, c_pad);
+    }
     return hipGetLastError();
 }
 

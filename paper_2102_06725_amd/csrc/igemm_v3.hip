@@ -1,0 +1,274 @@
+// igemm_v3.hip -- large-tile implicit-GEMM convolution for the forward pass
+// and each stride phase of the backward-data pass, for reductions whose
+// per-tap channel count is a multiple of 64 (every ResNet-50 layer but the
+// stem).
+//
+// Design (gfx950):
+//   - 4 waves per workgroup, block tile BM x BN with wave tiles up to
+//     128 x 128 built from v_mfma_f32_32x32x16 blocks: fewer LDS fragment
+//     reads and fewer global loads per matrix-core instruction;
+//   - 64-element k-slices staged straight from memory into LDS with
+//     buffer_load ... lds, STAGES deep, one barrier per slice;
+//   - per-lane load offsets are fixed for the whole kernel; the part that
+//     changes from slice to slice (tap and channel base) is uniform and is
+//     folded into the buffer descriptor's base address with scalar
+//     instructions, so a slice costs almost no vector ALU work;
+//   - zero padding: rows outside the GEMM get an out-of-range offset once;
+//     for padded convolutions each staged row carries a bitmask of the taps
+//     that land inside the image, tested per load.
+#include "launch.hpp"
+
+namespace nnconv {
+
+namespace v3 {
+
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
+}
+
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_barrier" ::: "memory"); }
+
+// Buffer descriptor for bytes [base + shift, base + bytes) (gfx9 format).
+__device__ __forceinline__ i32x4 desc_at(const void *base, uint32_t bytes, uint32_t shift) {
+    const uint64_t a = (uint64_t)base + shift;
+    i32x4 d;
+    d[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)a);
+    d[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(a >> 32) & 0xFFFFu));
+    d[2] = __builtin_amdgcn_readfirstlane((int32_t)(shift < bytes ? bytes - shift : 0u));
+    d[3] = 0x00020000;
+    return d;
+}
+
+// buffer_load_dwordx4 ... lds: lane i's 16 bytes go to LDS byte address
+// lds_addr + 16*i; offsets at or past the descriptor's range deliver zeros.
+__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 desc) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(desc)
+        : "memory");
+}
+
+// LDS tile: 8 x 16-byte chunks (128 bytes) per row; row r, logical chunk c
+// at slot r*8 + (c ^ swz(r)) with swz(r) = (r >> 1) & 7.  The 64 LDS banks
+// serve a 16-byte read for 16 lanes per cycle; a fragment read has 16
+// consecutive rows at one logical chunk, which this places in 16 distinct
+// 16-byte bank groups (row parity picks the 128-byte half, swz the chunk).
+__device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ int slot(int r, int c) { return r * 8 + (c ^ swz8(r)); }
+
+}  // namespace v3
+
+template <class T, int BM, int BN, int WM, int WN, int STAGES, bool PAD>
+__global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParams P) {
+    using namespace v3;
+    constexpr int NW = WM * WN;  // waves per workgroup
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int FM = WTM / 32, FN = WTN / 32;
+    constexpr int A_ROWS = BM / (8 * NW), B_ROWS = BN / (8 * NW);  // rows each thread stages
+    constexpr int A_SLOTS = BM * 8, B_SLOTS = BN * 8;
+    constexpr int STAGE_SLOTS = A_SLOTS + B_SLOTS;
+    constexpr int LOADS = A_ROWS + B_ROWS;
+    static_assert(FM >= 1 && FN >= 1 && A_ROWS >= 1 && B_ROWS >= 1, "tile shape");
+
+    __shared__ u32x4 lds[STAGES * STAGE_SLOTS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+
+    const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int per_g = P.tiles_m * P.tiles_n;
+    const int g = (int)lid / per_g;
+    const int rem = (int)lid - g * per_g;
+    const int tm = rem / P.tiles_n;
+    const int tn = rem - tm * P.tiles_n;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    // Staging role: a 64-lane load instruction covers 8 rows x 8 chunks;
+    // lane -> (row lane/8, physical chunk lane%8), so it fetches logical
+    // chunk (lane%8) ^ swz(row).
+    const int lrow = lane >> 3;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void *)&lds[0];
+
+    uint32_t a_voff[A_ROWS];
+    uint64_t a_mask[A_ROWS];
+#pragma unroll
+    for (int j = 0; j < A_ROWS; ++j) {
+        const int r = (wave * A_ROWS + j) * 8 + lrow;
+        const int lchunk = (lane & 7) ^ swz8(r);
+        const int m = m0 + r;
+        a_mask[j] = 0;
+        if (m < P.M) {
+            const int q1 = (int)fdiv((uint32_t)m, P.div_mj);
+            const int jj = m - q1 * P.mj;
+            const int n = (int)fdiv((uint32_t)q1, P.div_mi);
+            const int ii = q1 - n * P.mi;
+            const int bh = ii * P.ai_mul + P.ai_add;
+            const int bw = jj * P.aj_mul + P.aj_add;
+            // byte offset of channel 0 of this row's base pixel (may be negative
+            // for padded rows: only used together with a valid tap offset)
+            a_voff[j] = (uint32_t)(((n * P.a_h + bh) * P.a_w + bw) * P.a_c + g * P.a_cg_ofs) * 2u +
+                        (uint32_t)lchunk * 16u;
+            if constexpr (PAD) {
+                for (int t = 0; t < P.taps.n; ++t) {
+                    const int h = bh + P.taps.dh[t], w = bw + P.taps.dw[t];
+                    if ((unsigned)h < (unsigned)P.a_h && (unsigned)w < (unsigned)P.a_w)
+                        a_mask[j] |= (uint64_t)1 << t;
+                }
+            }
+        } else {
+            a_voff[j] = OOB_OFFSET;
+        }
+    }
+    uint32_t b_voff[B_ROWS];
+#pragma unroll
+    for (int j = 0; j < B_ROWS; ++j) {
+        const int r = (wave * B_ROWS + j) * 8 + lrow;
+        const int lchunk = (lane & 7) ^ swz8(r);
+        const int col = n0 + r;
+        b_voff[j] = col < P.ncols ? (uint32_t)(g * P.b_g_ofs + col * P.b_ld) * 2u + (uint32_t)lchunk * 16u
+                                  : OOB_OFFSET;
+    }
+
+    const int cpt = P.cr >> 6;  // 64-element slices per tap
+    int ld_t = 0, ld_c = 0;     // tap and channel base of the next slice to load
+
+    auto issue = [&](int buf) {
+        const int t = ld_t;
+        const uint32_t ashift = (uint32_t)(P.taps.dh[t] * P.a_w + P.taps.dw[t]) * (uint32_t)P.a_c * 2u;
+        // A: x / dy rows; the tap's pixel shift can be negative, so it is
+        // applied to the lane offsets (one add) rather than to the base
+        const i32x4 da = desc_at(P.a, P.a_bytes, (uint32_t)ld_c * 2u);
+        const i32x4 db = desc_at(P.b, P.b_bytes, (uint32_t)(P.taps.boff[t] + ld_c) * 2u);
+        const uint32_t sb = lds0 + (uint32_t)(buf * STAGE_SLOTS) * 16u;
+#pragma unroll
+        for (int j = 0; j < A_ROWS; ++j) {
+            uint32_t off = a_voff[j] + ashift;
+            if constexpr (PAD) {
+                if (!((a_mask[j] >> t) & 1)) off = OOB_OFFSET;
+            } else {
+                if (a_voff[j] == OOB_OFFSET) off = OOB_OFFSET;
+            }
+            dma16(sb + (uint32_t)((wave * A_ROWS + j) * 64) * 16u, off, da);
+        }
+#pragma unroll
+        for (int j = 0; j < B_ROWS; ++j)
+            dma16(sb + (uint32_t)(A_SLOTS + (wave * B_ROWS + j) * 64) * 16u, b_voff[j], db);
+        // taps inner, channel slices outer: the taps of one 64-channel slice
+        // re-read overlapping pixels back to back, while they are still in L2
+        if (++ld_t == P.taps.n) {
+            ld_t = 0;
+            ld_c += 64;
+        }
+    };
+
+    f32x16 acc[FN][FM];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) acc[j][i] = f32x16{};
+
+    const int l32 = lane & 31;
+    const int khalf = lane >> 5;
+    const int k_iters = P.taps.n * cpt;
+
+    if (k_iters > 0) {
+        const int pro = k_iters < STAGES - 1 ? k_iters : STAGES - 1;
+        for (int s = 0; s < pro; ++s) issue(s);
+        for (int kt = 0; kt < k_iters; ++kt) {
+            // slice kt has landed once at most (STAGES-2) later slices are pending
+            if (kt + STAGES - 2 < k_iters)
+                wait_vmcnt<(STAGES - 2) * LOADS>();
+            else
+                wait_vmcnt<0>();
+            barrier_lds();
+            if (kt + STAGES - 1 < k_iters) issue((kt + STAGES - 1) % STAGES);
+            const u32x4 *st = &lds[(kt % STAGES) * STAGE_SLOTS];
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const int kc = 2 * ks + khalf;
+                u32x4 fp[FM], fw[FN];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) fp[i] = st[slot(wm * WTM + i * 32 + l32, kc)];
+#pragma unroll
+                for (int j = 0; j < FN; ++j) fw[j] = st[A_SLOTS + slot(wn * WTN + j * 32 + l32, kc)];
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int i = 0; i < FM; ++i) acc[j][i] = mfma32<T>(fw[j], fp[i], acc[j][i]);
+            }
+        }
+    }
+
+    // Epilogue: lane holds pixel column l32 of each 32-pixel block and, for
+    // each 32-channel block, channels 8*e + 4*khalf + {0..3} (e = 0..3).
+    uint16_t *out = (uint16_t *)P.out;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int m = m0 + wm * WTM + i * 32 + l32;
+        if (m >= P.M) continue;
+        const int q1 = (int)fdiv((uint32_t)m, P.div_mj);
+        const int jj = m - q1 * P.mj;
+        const int n = (int)fdiv((uint32_t)q1, P.div_mi);
+        const int ii = q1 - n * P.mi;
+        const int oh = ii * P.oi_mul + P.oi_add;
+        const int ow = jj * P.oj_mul + P.oj_add;
+        const int64_t obase =
+            ((int64_t)(n * P.o_h + oh) * P.o_w + ow) * P.o_c + (int64_t)g * P.o_cg_ofs;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int ch = n0 + wn * WTN + j * 32 + 8 * e + 4 * khalf;
+                if (ch >= P.ncols) continue;
+                u32x2 pk;
+                pk[0] = to16<T>(acc[j][i][4 * e + 0] * P.alpha) |
+                        (to16<T>(acc[j][i][4 * e + 1] * P.alpha) << 16);
+                pk[1] = to16<T>(acc[j][i][4 * e + 2] * P.alpha) |
+                        (to16<T>(acc[j][i][4 * e + 3] * P.alpha) << 16);
+                *(u32x2 *)(out + obase + ch) = pk;
+            }
+        }
+    }
+}
+
+template <class T, int BM, int BN, int WM, int WN, int STAGES>
+static hipError_t launch_v3_cfg(TNParams &p, bool pad, hipStream_t st) {
+    p.tiles_m = (p.M + BM - 1) / BM;
+    p.tiles_n = (p.ncols + BN - 1) / BN;
+    const int64_t nb = (int64_t)p.tiles_m * p.tiles_n * p.groups;
+    if (nb <= 0) return hipSuccess;
+    if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (pad)
+        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, STAGES, true>), dim3((uint32_t)nb),
+                           dim3(WM * WN * 64), 0, st, p);
+    else
+        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, STAGES, false>), dim3((uint32_t)nb),
+                           dim3(WM * WN * 64), 0, st, p);
+    return hipGetLastError();
+}
+
+template <class T>
+static hipError_t launch_v3_t(V3Config cfg, TNParams &p, bool pad, hipStream_t st) {
+    switch (cfg) {
+        case V3_256x256: return launch_v3_cfg<T, 256, 256, 2, 4, 2>(p, pad, st);
+        case V3_256x128: return launch_v3_cfg<T, 256, 128, 4, 2, 3>(p, pad, st);
+        case V3_256x64:
+        default: return launch_v3_cfg<T, 256, 64, 4, 2, 3>(p, pad, st);
+    }
+}
+
+hipError_t launch_igemm_v3(int dtype, V3Config cfg, TNParams &p, bool pad, hipStream_t st) {
+    if (dtype == Half::id) return launch_v3_t<Half>(cfg, p, pad, st);
+    return launch_v3_t<BFloat>(cfg, p, pad, st);
+}
+
+}  // namespace nnconv

@@ -59,6 +59,14 @@ struct TNParams {
 enum TNConfig { TN_128x128 = 0, TN_256x64 = 1, TN_256x128 = 2 };
 
 hipError_t launch_igemm_tn(int dtype, TNConfig cfg, TNParams &p, hipStream_t st);
+// Same GEMM with the multi-stage direct-to-LDS pipeline (recomputes k_iters
+// for its own slice depth).
+hipError_t launch_igemm_dma(int dtype, TNConfig cfg, TNParams &p, hipStream_t st);
+
+// Large-tile variant for cr % 64 == 0 (k_iters is derived from the taps).
+// pad: some (row, tap) pairs fall outside the A image and must read zeros.
+enum V3Config { V3_256x256 = 0, V3_256x128 = 1, V3_256x64 = 2 };
+hipError_t launch_igemm_v3(int dtype, V3Config cfg, TNParams &p, bool pad, hipStream_t st);
 
 // Backward-weight split-K partial sums:
 //   ws[split][k][j] = sum over pixels of this split of dy[pix, k] * xcol[pix, j]

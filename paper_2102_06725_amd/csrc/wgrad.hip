@@ -246,27 +246,41 @@ __device__ __forceinline__ bool reduce_store(float sum, int64_t e, void *dw, flo
     }
 }
 
-// Sums the split partials in increasing split order (fixed order: results
-// are bitwise reproducible), then applies the loss-scale step.  VEC: count
-// is a multiple of 4 and each thread handles 4 consecutive elements.
+// Sums the split partials in a fixed order (results are bitwise
+// reproducible), then applies the loss-scale step.
+//
+// VEC (count a multiple of 4): a workgroup owns 64 consecutive elements
+// (16 float4 columns); its 256 threads are 16 columns x 16 split lanes.
+// Split lane l adds splits l, l+16, l+32, ... in increasing order, then lane
+// 0 adds the 16 lane sums in increasing lane order.  The many independent
+// loads in flight keep the reduction bandwidth-bound even when there are
+// few output elements and many splits.
 template <int OUT, bool VEC>
 __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *__restrict__ ws,
                                                            int32_t splits, int64_t count,
                                                            void *dw, float inv_scale,
                                                            int accumulate, int32_t *flag,
                                                            int kcrs, int32_t cg, int32_t rs) {
-    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
     bool bad = false;
     if constexpr (VEC) {
-        const int64_t e4 = t * 4;
-        if (e4 >= count) return;
+        __shared__ f32x4 part[16][16];
+        const int col = threadIdx.x & 15, sl = threadIdx.x >> 4;
+        const int64_t e4 = (int64_t)blockIdx.x * 64 + col * 4;
         f32x4 sum = f32x4{};
-        for (int sp = 0; sp < splits; ++sp)
-            sum += *(const f32x4 *)(ws + (int64_t)sp * count + e4);
+        if (e4 < count)
+            for (int sp = sl; sp < splits; sp += 16)
+                sum += *(const f32x4 *)(ws + (int64_t)sp * count + e4);
+        part[sl][col] = sum;
+        __syncthreads();
+        if (sl != 0 || e4 >= count) return;
+        f32x4 tot = part[0][col];
+#pragma unroll
+        for (int l = 1; l < 16; ++l) tot += part[l][col];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-            bad |= reduce_store<OUT>(sum[u], e4 + u, dw, inv_scale, accumulate, kcrs, cg, rs);
+            bad |= reduce_store<OUT>(tot[u], e4 + u, dw, inv_scale, accumulate, kcrs, cg, rs);
     } else {
+        const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
         if (t >= count) return;
         float sum = 0.f;
         for (int sp = 0; sp < splits; ++sp) sum += ws[(int64_t)sp * count + t];
@@ -280,7 +294,7 @@ static void launch_reduce_out(const float *ws, int32_t splits, int64_t count, vo
                               float inv_scale, int accumulate, int32_t *flag, int kcrs, int32_t cg,
                               int32_t rs, hipStream_t st) {
     if (count % 4 == 0) {
-        const int64_t nb = (count / 4 + 255) / 256;
+        const int64_t nb = (count + 63) / 64;
         hipLaunchKernelGGL((wgrad_reduce_kernel<OUT, true>), dim3((uint32_t)nb), dim3(256), 0, st,
                            ws, splits, count, dw, inv_scale, accumulate, flag, kcrs, cg, rs);
     } else {

@@ -71,6 +71,11 @@ SMALL = [
     ("direct: groups Cg=4", Case(L("q", 2, 16, 8, 8, 16, 3, 3, 1, 1, groups=4))),
     ("direct: NCHW C12 bf16", Case(L("r", 2, 12, 7, 9, 20, 3, 3, 2, 1), layout="nchw",
                                    dtype=I.BF16)),
+    ("3x3 s2 C64 K64 (large-tile phases)", Case(L("s2", 3, 64, 15, 13, 64, 3, 3, 2, 1))),
+    ("1x1 s2 C64 K64", Case(L("s3", 2, 64, 14, 15, 64, 1, 1, 2, 0))),
+    ("3x3 C128 K256 ragged M", Case(L("s4", 3, 128, 9, 11, 256, 3, 3, 1, 1))),
+    ("1x1 C256 K320", Case(L("s5", 2, 256, 9, 7, 320, 1, 1))),
+    ("3x3 pad 0 C64", Case(L("s6", 2, 64, 9, 8, 128, 3, 3, 1, 0))),
     ("P = Q = 1", Case(L("s", 2, 16, 3, 3, 16, 3, 3, 1, 0))),
     ("H = W = 1, 1x1", Case(L("t", 5, 32, 1, 1, 24, 1, 1))),
 ]

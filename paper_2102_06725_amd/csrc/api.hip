@@ -205,7 +205,17 @@ TNParams tn_base() {
 
 TNConfig pick_tn(int64_t ncols) { return ncols <= 64 ? TN_256x64 : TN_128x128; }
 
-V3Config pick_v3(int64_t ncols) {
+// Tile configuration from the output width and the reduction length
+// (taps x channels): reductions of at most SHORT_RED elements use the
+// single-stage tiles, several of which share a CU.
+constexpr int64_t SHORT_RED = 1024;
+
+V3Config pick_v3(int64_t ncols, int64_t red) {
+    if (red <= SHORT_RED) {
+        if (ncols <= 64) return V3S_256x64;
+        if (ncols <= 128) return V3S_256x128;
+        return V3S_128x256;
+    }
     if (ncols <= 64) return V3_256x64;
     if (ncols <= 128) return V3_256x128;
     return V3_256x256;
@@ -219,6 +229,7 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     p.b = w;
     p.b_bytes = (uint32_t)(G.k * G.r * G.s * G.cg * 2);
     p.out = y;
+    p.o_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
     p.mi = (int32_t)G.p;
     p.mj = (int32_t)G.q;
     p.M = (int32_t)(G.n * G.p * G.q);
@@ -248,7 +259,7 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     p.taps.n = t;
     p.k_iters = (int32_t)((int64_t(t) * G.cg + 63) / 64);
     if (G.cg % 64 == 0)
-        return hip_status(launch_igemm_v3(G.dtype, pick_v3(G.kg), p, G.ph > 0 || G.pw > 0, st));
+        return hip_status(launch_igemm_v3(G.dtype, pick_v3(G.kg, (int64_t)p.taps.n * G.cg), p, G.ph > 0 || G.pw > 0, st));
     return hip_status(launch_igemm_dma(G.dtype, pick_tn(G.kg), p, st));
 }
 
@@ -268,6 +279,7 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             p.b = wt;
             p.b_bytes = (uint32_t)(G.k * G.r * G.s * G.cg * 2);
             p.out = dx;
+            p.o_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
             p.mi = (int32_t)mi;
             p.mj = (int32_t)mj;
             p.M = (int32_t)(G.n * mi * mj);
@@ -304,7 +316,7 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             p.k_iters = (int32_t)((int64_t(t) * G.kg + 63) / 64);
             const bool pad = !(G.r == 1 && G.s == 1 && G.ph == 0 && G.pw == 0);
             if (G.kg % 64 == 0)
-                TRY_HIP(launch_igemm_v3(G.dtype, pick_v3(G.cg), p, pad, st));
+                TRY_HIP(launch_igemm_v3(G.dtype, pick_v3(G.cg, (int64_t)t * G.kg), p, pad, st));
             else
                 TRY_HIP(launch_igemm_dma(G.dtype, pick_tn(G.cg), p, st));
         }

@@ -4,11 +4,13 @@
 // stem).
 //
 // Design (gfx950):
-//   - 4 waves per workgroup, block tile BM x BN with wave tiles up to
-//     128 x 128 built from v_mfma_f32_32x32x16 blocks: fewer LDS fragment
-//     reads and fewer global loads per matrix-core instruction;
-//   - 64-element k-slices staged straight from memory into LDS with
-//     buffer_load ... lds, STAGES deep, one barrier per slice;
+//   - block tile BM x BN, NW = WM x WN waves, wave tiles built from
+//     v_mfma_f32_32x32x16 blocks (up to 128 x 64 per wave): few LDS fragment
+//     reads and few global loads per matrix-core instruction;
+//   - k-slices of BKC x 8 reduction elements staged straight from memory
+//     into LDS with buffer_load ... lds, STAGES deep, one barrier per slice;
+//     configurations are sized so two workgroups share a CU, so one
+//     workgroup's barrier wait is covered by the other's MFMAs;
 //   - per-lane load offsets are fixed for the whole kernel; the part that
 //     changes from slice to slice (tap and channel base) is uniform and is
 //     folded into the buffer descriptor's base address with scalar
@@ -55,29 +57,41 @@ __device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 de
         : "memory");
 }
 
-// LDS tile: 8 x 16-byte chunks (128 bytes) per row; row r, logical chunk c
-// at slot r*8 + (c ^ swz(r)) with swz(r) = (r >> 1) & 7.  The 64 LDS banks
-// serve a 16-byte read for 16 lanes per cycle; a fragment read has 16
-// consecutive rows at one logical chunk, which this places in 16 distinct
-// 16-byte bank groups (row parity picks the 128-byte half, swz the chunk).
-__device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
-__device__ __forceinline__ int slot(int r, int c) { return r * 8 + (c ^ swz8(r)); }
+// LDS tile: BKC 16-byte chunks per row; row r, logical chunk c at slot
+// r*BKC + (c ^ swz(r)).  The 64 LDS banks serve a 16-byte read for 16 lanes
+// per cycle, and a fragment read has 16 consecutive rows at one logical
+// chunk: the swizzle spreads them over 16 distinct 16-byte bank groups
+// (128-byte rows: parity picks the half, (r>>1)&7 the chunk; 64-byte rows:
+// r&3 picks the quarter, (r>>2)&3 the chunk).
+template <int BKC>
+__device__ __forceinline__ int swz(int r) {
+    return BKC == 8 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+}
+template <int BKC>
+__device__ __forceinline__ int slot(int r, int c) {
+    return r * BKC + (c ^ swz<BKC>(r));
+}
 
 }  // namespace v3
 
-template <class T, int BM, int BN, int WM, int WN, int STAGES, bool PAD>
-__global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParams P) {
+template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool PAD>
+__global__ __launch_bounds__(WM * WN * 64, (WM * WN == 4) ? ((BM * BN <= 128 * 128) ? 4 : 2) : 1)
+void igemm_v3_kernel(const TNParams P) {
     using namespace v3;
-    constexpr int NW = WM * WN;  // waves per workgroup
+    constexpr int NW = WM * WN;             // waves per workgroup
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int FM = WTM / 32, FN = WTN / 32;
-    constexpr int A_ROWS = BM / (8 * NW), B_ROWS = BN / (8 * NW);  // rows each thread stages
-    constexpr int A_SLOTS = BM * 8, B_SLOTS = BN * 8;
+    constexpr int BK = BKC * 8;             // reduction elements per slice
+    constexpr int RPI = 64 / BKC;           // rows covered by one 64-lane load
+    constexpr int A_LD = BM / (RPI * NW);   // loads per thread per slice (A)
+    constexpr int B_LD = BN / (RPI * NW);   // loads per thread per slice (B)
+    constexpr int A_SLOTS = BM * BKC, B_SLOTS = BN * BKC;
     constexpr int STAGE_SLOTS = A_SLOTS + B_SLOTS;
-    constexpr int LOADS = A_ROWS + B_ROWS;
-    static_assert(FM >= 1 && FN >= 1 && A_ROWS >= 1 && B_ROWS >= 1, "tile shape");
+    constexpr int LOADS = A_LD + B_LD;
+    static_assert(FM >= 1 && FN >= 1 && A_LD >= 1 && B_LD >= 1, "tile shape");
 
-    __shared__ u32x4 lds[STAGES * STAGE_SLOTS];
+    constexpr int LDS_SLOTS = STAGES * STAGE_SLOTS > BM * BN / 8 ? STAGES * STAGE_SLOTS : BM * BN / 8;
+    __shared__ u32x4 lds[LDS_SLOTS];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -92,18 +106,18 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParam
     const int tn = rem - tm * P.tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // Staging role: a 64-lane load instruction covers 8 rows x 8 chunks;
-    // lane -> (row lane/8, physical chunk lane%8), so it fetches logical
-    // chunk (lane%8) ^ swz(row).
-    const int lrow = lane >> 3;
+    // Staging role: load j of this wave fills rows (wave*LD + j)*RPI + lane/BKC,
+    // physical chunk lane%BKC, i.e. logical chunk (lane%BKC) ^ swz(row).
+    const int lrow = lane / BKC;
+    const int pch = lane & (BKC - 1);
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void *)&lds[0];
 
-    uint32_t a_voff[A_ROWS];
-    uint64_t a_mask[A_ROWS];
+    uint32_t a_voff[A_LD];
+    uint64_t a_mask[A_LD];
 #pragma unroll
-    for (int j = 0; j < A_ROWS; ++j) {
-        const int r = (wave * A_ROWS + j) * 8 + lrow;
-        const int lchunk = (lane & 7) ^ swz8(r);
+    for (int j = 0; j < A_LD; ++j) {
+        const int r = (wave * A_LD + j) * RPI + lrow;
+        const int lchunk = pch ^ swz<BKC>(r);
         const int m = m0 + r;
         a_mask[j] = 0;
         if (m < P.M) {
@@ -113,8 +127,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParam
             const int ii = q1 - n * P.mi;
             const int bh = ii * P.ai_mul + P.ai_add;
             const int bw = jj * P.aj_mul + P.aj_add;
-            // byte offset of channel 0 of this row's base pixel (may be negative
-            // for padded rows: only used together with a valid tap offset)
+            // byte offset of this row's base pixel and chunk (may wrap below 0
+            // for padded rows: only used together with a valid tap shift)
             a_voff[j] = (uint32_t)(((n * P.a_h + bh) * P.a_w + bw) * P.a_c + g * P.a_cg_ofs) * 2u +
                         (uint32_t)lchunk * 16u;
             if constexpr (PAD) {
@@ -128,45 +142,46 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParam
             a_voff[j] = OOB_OFFSET;
         }
     }
-    uint32_t b_voff[B_ROWS];
+    uint32_t b_voff[B_LD];
 #pragma unroll
-    for (int j = 0; j < B_ROWS; ++j) {
-        const int r = (wave * B_ROWS + j) * 8 + lrow;
-        const int lchunk = (lane & 7) ^ swz8(r);
+    for (int j = 0; j < B_LD; ++j) {
+        const int r = (wave * B_LD + j) * RPI + lrow;
+        const int lchunk = pch ^ swz<BKC>(r);
         const int col = n0 + r;
-        b_voff[j] = col < P.ncols ? (uint32_t)(g * P.b_g_ofs + col * P.b_ld) * 2u + (uint32_t)lchunk * 16u
-                                  : OOB_OFFSET;
+        b_voff[j] = col < P.ncols
+                        ? (uint32_t)(g * P.b_g_ofs + col * P.b_ld) * 2u + (uint32_t)lchunk * 16u
+                        : OOB_OFFSET;
     }
 
-    const int cpt = P.cr >> 6;  // 64-element slices per tap
-    int ld_t = 0, ld_c = 0;     // tap and channel base of the next slice to load
+    int ld_t = 0, ld_c = 0;  // tap and channel base of the next slice to load
 
     auto issue = [&](int buf) {
         const int t = ld_t;
-        const uint32_t ashift = (uint32_t)(P.taps.dh[t] * P.a_w + P.taps.dw[t]) * (uint32_t)P.a_c * 2u;
         // A: x / dy rows; the tap's pixel shift can be negative, so it is
-        // applied to the lane offsets (one add) rather than to the base
+        // added to the lane offsets; the channel base moves the descriptor
+        const uint32_t ashift =
+            (uint32_t)(P.taps.dh[t] * P.a_w + P.taps.dw[t]) * (uint32_t)P.a_c * 2u;
         const i32x4 da = desc_at(P.a, P.a_bytes, (uint32_t)ld_c * 2u);
         const i32x4 db = desc_at(P.b, P.b_bytes, (uint32_t)(P.taps.boff[t] + ld_c) * 2u);
         const uint32_t sb = lds0 + (uint32_t)(buf * STAGE_SLOTS) * 16u;
 #pragma unroll
-        for (int j = 0; j < A_ROWS; ++j) {
+        for (int j = 0; j < A_LD; ++j) {
             uint32_t off = a_voff[j] + ashift;
             if constexpr (PAD) {
                 if (!((a_mask[j] >> t) & 1)) off = OOB_OFFSET;
             } else {
                 if (a_voff[j] == OOB_OFFSET) off = OOB_OFFSET;
             }
-            dma16(sb + (uint32_t)((wave * A_ROWS + j) * 64) * 16u, off, da);
+            dma16(sb + (uint32_t)((wave * A_LD + j) * 64) * 16u, off, da);
         }
 #pragma unroll
-        for (int j = 0; j < B_ROWS; ++j)
-            dma16(sb + (uint32_t)(A_SLOTS + (wave * B_ROWS + j) * 64) * 16u, b_voff[j], db);
-        // taps inner, channel slices outer: the taps of one 64-channel slice
+        for (int j = 0; j < B_LD; ++j)
+            dma16(sb + (uint32_t)(A_SLOTS + (wave * B_LD + j) * 64) * 16u, b_voff[j], db);
+        // taps inner, channel slices outer: the taps of one channel slice
         // re-read overlapping pixels back to back, while they are still in L2
         if (++ld_t == P.taps.n) {
             ld_t = 0;
-            ld_c += 64;
+            ld_c += BK;
         }
     };
 
@@ -178,9 +193,36 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParam
 
     const int l32 = lane & 31;
     const int khalf = lane >> 5;
-    const int k_iters = P.taps.n * cpt;
+    const int k_iters = P.taps.n * (P.cr / BK);
 
-    if (k_iters > 0) {
+    auto compute = [&](const u32x4 *st) {
+#pragma unroll
+        for (int ks = 0; ks < BKC / 2; ++ks) {
+            const int kc = 2 * ks + khalf;
+            u32x4 fp[FM], fw[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) fp[i] = st[slot<BKC>(wm * WTM + i * 32 + l32, kc)];
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                fw[j] = st[A_SLOTS + slot<BKC>(wn * WTN + j * 32 + l32, kc)];
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int i = 0; i < FM; ++i) acc[j][i] = mfma32<T>(fw[j], fp[i], acc[j][i]);
+        }
+    };
+
+    if constexpr (STAGES == 1) {
+        // short reductions: no pipeline; several resident workgroups per CU
+        // overlap each other's loads, MFMAs and stores instead
+        for (int kt = 0; kt < k_iters; ++kt) {
+            if (kt > 0) barrier_lds();  // previous slice fully read
+            issue(0);
+            wait_vmcnt<0>();
+            barrier_lds();
+            compute(&lds[0]);
+        }
+    } else if (k_iters > 0) {
         const int pro = k_iters < STAGES - 1 ? k_iters : STAGES - 1;
         for (int s = 0; s < pro; ++s) issue(s);
         for (int kt = 0; kt < k_iters; ++kt) {
@@ -191,30 +233,49 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParam
                 wait_vmcnt<0>();
             barrier_lds();
             if (kt + STAGES - 1 < k_iters) issue((kt + STAGES - 1) % STAGES);
-            const u32x4 *st = &lds[(kt % STAGES) * STAGE_SLOTS];
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const int kc = 2 * ks + khalf;
-                u32x4 fp[FM], fw[FN];
-#pragma unroll
-                for (int i = 0; i < FM; ++i) fp[i] = st[slot(wm * WTM + i * 32 + l32, kc)];
-#pragma unroll
-                for (int j = 0; j < FN; ++j) fw[j] = st[A_SLOTS + slot(wn * WTN + j * 32 + l32, kc)];
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-#pragma unroll
-                    for (int i = 0; i < FM; ++i) acc[j][i] = mfma32<T>(fw[j], fp[i], acc[j][i]);
-            }
+            compute(&lds[(kt % STAGES) * STAGE_SLOTS]);
         }
     }
 
-    // Epilogue: lane holds pixel column l32 of each 32-pixel block and, for
-    // each 32-channel block, channels 8*e + 4*khalf + {0..3} (e = 0..3).
-    uint16_t *out = (uint16_t *)P.out;
+    // Epilogue through LDS: the tile is converted to 16-bit and written to
+    // LDS as [BM pixel rows][BN channels] (16-byte chunks swizzled by row),
+    // then read back a 16-byte chunk per lane, consecutive lanes along a row,
+    // so every global store writes whole cache lines of one output pixel.
+    // Lane (MFMA layout) holds pixel l32 of each 32-pixel block and, of each
+    // 32-channel block, channels 8*e + 4*khalf + {0..3} (e = 0..3).
+    constexpr int CPR = BN / 8;                    // 16-byte chunks per tile row
+    constexpr int CSW = CPR < 16 ? CPR - 1 : 15;   // chunk swizzle mask
+    static_assert(BM * BN / 8 <= LDS_SLOTS, "C tile must fit in LDS");
+    barrier_lds();  // every wave is done reading the last k-slice
+    {
+        char *cl = (char *)&lds[0];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = m0 + wm * WTM + i * 32 + l32;
-        if (m >= P.M) continue;
+        for (int i = 0; i < FM; ++i) {
+            const int r = wm * WTM + i * 32 + l32;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int c = (wn * WTN + j * 32) / 8 + e;
+                    u32x2 pk;
+                    pk[0] = to16<T>(acc[j][i][4 * e + 0] * P.alpha) |
+                            (to16<T>(acc[j][i][4 * e + 1] * P.alpha) << 16);
+                    pk[1] = to16<T>(acc[j][i][4 * e + 2] * P.alpha) |
+                            (to16<T>(acc[j][i][4 * e + 3] * P.alpha) << 16);
+                    *(u32x2 *)(cl + (r * CPR + (c ^ (r & CSW))) * 16 + khalf * 8) = pk;
+                }
+            }
+        }
+    }
+    barrier_lds();
+    uint16_t *out = (uint16_t *)P.out;
+    constexpr int ROWS_PER_PASS = NW * 64 / CPR;
+#pragma unroll 4
+    for (int r = tid / CPR; r < BM; r += ROWS_PER_PASS) {
+        const int c = tid % CPR;
+        const int m = m0 + r;
+        const int ch = n0 + c * 8;
+        if (m >= P.M || ch >= P.ncols) continue;
         const int q1 = (int)fdiv((uint32_t)m, P.div_mj);
         const int jj = m - q1 * P.mj;
         const int n = (int)fdiv((uint32_t)q1, P.div_mi);
@@ -223,24 +284,11 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void igemm_v3_kernel(const TNParam
         const int ow = jj * P.oj_mul + P.oj_add;
         const int64_t obase =
             ((int64_t)(n * P.o_h + oh) * P.o_w + ow) * P.o_c + (int64_t)g * P.o_cg_ofs;
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int ch = n0 + wn * WTN + j * 32 + 8 * e + 4 * khalf;
-                if (ch >= P.ncols) continue;
-                u32x2 pk;
-                pk[0] = to16<T>(acc[j][i][4 * e + 0] * P.alpha) |
-                        (to16<T>(acc[j][i][4 * e + 1] * P.alpha) << 16);
-                pk[1] = to16<T>(acc[j][i][4 * e + 2] * P.alpha) |
-                        (to16<T>(acc[j][i][4 * e + 3] * P.alpha) << 16);
-                *(u32x2 *)(out + obase + ch) = pk;
-            }
-        }
+        *(u32x4 *)(out + obase + ch) = lds[r * CPR + (c ^ (r & CSW))];
     }
 }
 
-template <class T, int BM, int BN, int WM, int WN, int STAGES>
+template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES>
 static hipError_t launch_v3_cfg(TNParams &p, bool pad, hipStream_t st) {
     p.tiles_m = (p.M + BM - 1) / BM;
     p.tiles_n = (p.ncols + BN - 1) / BN;
@@ -248,21 +296,32 @@ static hipError_t launch_v3_cfg(TNParams &p, bool pad, hipStream_t st) {
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (pad)
-        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, STAGES, true>), dim3((uint32_t)nb),
-                           dim3(WM * WN * 64), 0, st, p);
+        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, BKC, STAGES, true>),
+                           dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     else
-        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, STAGES, false>), dim3((uint32_t)nb),
-                           dim3(WM * WN * 64), 0, st, p);
+        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, BKC, STAGES, false>),
+                           dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
 
+// Configurations (LDS per workgroup in parentheses; <= 80 KB lets two
+// workgroups share a CU):
+//   256x256: 8 waves of 128x64, 64-element slices, 2 stages (128 KB)
+//   256x128: 4 waves of 128x64, 32-element slices, 3 stages (72 KB)
+//   256x64 : 4 waves of  64x64, 32-element slices, 3 stages (60 KB)
+// Short reductions (a few 64-element slices) use single-stage tiles whose
+// small LDS footprint lets 3-5 workgroups share a CU:
+//   128x128: 4 waves of 64x64 (32 KB);  128x64: 4 waves of 64x32 (24 KB)
 template <class T>
 static hipError_t launch_v3_t(V3Config cfg, TNParams &p, bool pad, hipStream_t st) {
     switch (cfg) {
-        case V3_256x256: return launch_v3_cfg<T, 256, 256, 2, 4, 2>(p, pad, st);
-        case V3_256x128: return launch_v3_cfg<T, 256, 128, 4, 2, 3>(p, pad, st);
+        case V3_256x256: return launch_v3_cfg<T, 256, 256, 2, 4, 8, 2>(p, pad, st);
+        case V3_256x128: return launch_v3_cfg<T, 256, 128, 2, 2, 4, 3>(p, pad, st);
+        case V3S_128x256:
+        case V3S_256x128: return launch_v3_cfg<T, 128, 128, 2, 2, 8, 1>(p, pad, st);
+        case V3S_256x64: return launch_v3_cfg<T, 128, 64, 2, 2, 8, 1>(p, pad, st);
         case V3_256x64:
-        default: return launch_v3_cfg<T, 256, 64, 4, 2, 3>(p, pad, st);
+        default: return launch_v3_cfg<T, 256, 64, 4, 1, 4, 3>(p, pad, st);
     }
 }
 

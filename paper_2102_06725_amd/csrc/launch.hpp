@@ -38,6 +38,7 @@ struct TNParams {
     const void *b;
     uint32_t b_bytes;
     void *out;
+    uint32_t o_bytes;     // size of the output tensor in bytes
     int32_t M;
     int32_t mi, mj;
     FastDiv div_mj, div_mi;
@@ -65,7 +66,9 @@ hipError_t launch_igemm_dma(int dtype, TNConfig cfg, TNParams &p, hipStream_t st
 
 // Large-tile variant for cr % 64 == 0 (k_iters is derived from the taps).
 // pad: some (row, tap) pairs fall outside the A image and must read zeros.
-enum V3Config { V3_256x256 = 0, V3_256x128 = 1, V3_256x64 = 2 };
+enum V3Config { V3_256x256 = 0, V3_256x128 = 1, V3_256x64 = 2,
+                // single-stage variants for reductions of a few 64-element slices
+                V3S_128x256 = 3, V3S_256x128 = 4, V3S_256x64 = 5 };
 hipError_t launch_igemm_v3(int dtype, V3Config cfg, TNParams &p, bool pad, hipStream_t st);
 
 // Backward-weight split-K partial sums:

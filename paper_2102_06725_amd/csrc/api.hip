@@ -76,16 +76,25 @@ struct WgPlan {
     int32_t splits, pix_per_split;
 };
 
+WGConfig pick_wg(int64_t kg, int64_t rscg) {
+    if (kg <= 64) return WG_64x128;
+    if (kg <= 128) return rscg >= 256 ? WG_128x256 : WG_128x128;
+    return rscg >= 256 ? WG_256x256 : WG_256x128;
+}
+
 WgPlan plan_wgrad_fast(const Geom &G) {
     WgPlan pl;
-    const int64_t bmk = G.kg <= 64 ? 64 : 128, bnj = 128;
-    pl.cfg = G.kg <= 64 ? WG_64x128 : WG_128x128;
     const int64_t rscg = G.r * G.s * G.cg;
+    pl.cfg = pick_wg(G.kg, rscg);
+    static const int64_t tile_m[] = {128, 64, 256, 128, 256};
+    static const int64_t tile_n[] = {128, 128, 128, 256, 256};
+    const int64_t bmk = tile_m[pl.cfg], bnj = tile_n[pl.cfg];
     const int64_t tiles = G.g * ((G.kg + bmk - 1) / bmk) * ((rscg + bnj - 1) / bnj);
     const int64_t npq = G.n * G.p * G.q;
-    const int64_t iters = (npq + 63) / 64;
-    int64_t splits = (512 + tiles - 1) / tiles;
-    int64_t max_splits = iters / 4;  // at least 4 pixel slices per split
+    const int64_t iters = (npq + 63) / 64;  // 64-pixel units
+    const int64_t target = 512;
+    int64_t splits = (target + tiles - 1) / tiles;
+    int64_t max_splits = iters / 4;  // at least 256 pixels per split
     if (max_splits < 1) max_splits = 1;
     if (splits > max_splits) splits = max_splits;
     if (splits > 1024) splits = 1024;
@@ -347,7 +356,7 @@ nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *pa
     p.groups = (int32_t)G.g;
     p.splits = pl.splits;
     p.pix_per_split = pl.pix_per_split;
-    TRY_HIP(launch_wgrad_splitk(G.dtype, pl.cfg, p, st));
+    TRY_HIP(launch_wgrad_v2(G.dtype, pl.cfg, p, st));
     return NNCONV_OK;
 }
 

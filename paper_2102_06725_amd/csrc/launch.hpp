@@ -90,9 +90,12 @@ struct WGParams {
     int32_t tiles_m, tiles_n;   // filled by the launcher
 };
 
-enum WGConfig { WG_128x128 = 0, WG_64x128 = 1 };
+enum WGConfig { WG_128x128 = 0, WG_64x128 = 1, WG_256x128 = 2, WG_128x256 = 3, WG_256x256 = 4 };
 
 hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);
+// Same partial sums with direct-to-LDS pixel-major staging and transposing
+// LDS reads (pix_per_split must be a multiple of 32).
+hipError_t launch_wgrad_v2(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);
 
 // dw[e'] = (accumulate ? dw[e'] : 0) + inv_scale * sum_{s < splits} ws[s][e]
 // over e < count = K * R*S*Cg; e' = e for [K][R][S][Cg] output, or the

@@ -76,6 +76,8 @@ SMALL = [
     ("3x3 C128 K256 ragged M", Case(L("s4", 3, 128, 9, 11, 256, 3, 3, 1, 1))),
     ("1x1 C256 K320", Case(L("s5", 2, 256, 9, 7, 320, 1, 1))),
     ("3x3 pad 0 C64", Case(L("s6", 2, 64, 9, 8, 128, 3, 3, 1, 0))),
+    ("1x1 C192 K96", Case(L("s7", 2, 192, 7, 9, 96, 1, 1))),
+    ("3x3 C256 K512 bf16", Case(L("s8", 2, 256, 6, 5, 512, 3, 3, 1, 1), dtype=I.BF16)),
     ("P = Q = 1", Case(L("s", 2, 16, 3, 3, 16, 3, 3, 1, 0))),
     ("H = W = 1, 1x1", Case(L("t", 5, 32, 1, 1, 24, 1, 1))),
 ]

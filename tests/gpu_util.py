@@ -33,18 +33,21 @@ def to_dev(bits: np.ndarray):
 class Guarded:
     """A device buffer of `numel` elements with guard bands on both sides."""
 
-    def __init__(self, numel: int, fp32: bool = False, init: np.ndarray | None = None):
+    def __init__(self, numel: int, fp32: bool = False, init: np.ndarray | None = None,
+                 shift: int = 0):
+        """`shift` elements move the start off 16-byte alignment."""
         t = torch()
         self.fp32 = fp32
         self.numel = numel
+        self.lo = GUARD + shift
         if fp32:
-            host = np.full(numel + 2 * GUARD, CANARY32, np.uint32)
+            host = np.full(numel + 2 * GUARD + shift, CANARY32, np.uint32)
         else:
-            host = np.full(numel + 2 * GUARD, CANARY16, np.uint16)
+            host = np.full(numel + 2 * GUARD + shift, CANARY16, np.uint16)
         if init is not None:
-            host[GUARD:GUARD + numel] = np.ascontiguousarray(init).ravel().view(host.dtype)
+            host[self.lo:self.lo + numel] = np.ascontiguousarray(init).ravel().view(host.dtype)
         self.buf = t.from_numpy(host.view(np.int32 if fp32 else np.int16)).to("cuda")
-        self.view = self.buf[GUARD:GUARD + numel]
+        self.view = self.buf[self.lo:self.lo + numel]
 
     def ptr(self) -> int:
         return self.view.data_ptr()
@@ -53,8 +56,9 @@ class Guarded:
         h = self.buf.cpu().numpy()
         h = h.view(np.uint32 if self.fp32 else np.uint16)
         c = CANARY32 if self.fp32 else CANARY16
-        assert np.all(h[:GUARD] == c) and np.all(h[GUARD + self.numel:] == c), "guard band overwritten"
-        return h[GUARD:GUARD + self.numel]
+        assert np.all(h[:self.lo] == c) and np.all(h[self.lo + self.numel:] == c), \
+            "guard band overwritten"
+        return h[self.lo:self.lo + self.numel]
 
 
 @dataclasses.dataclass
@@ -122,7 +126,7 @@ def stream():
 
 
 def run_gpu(case: Case, t, passes=("fwd", "dgrad", "wgrad"), dw_dtype=None, inv_scale=None,
-            accumulate=0, dw_old=None, flag=None):
+            accumulate=0, dw_old=None, flag=None, dw_shift=0):
     """Run the requested passes on the GPU; returns dict of output bits /
     fp32 values in the case's layout."""
     L = case.layer
@@ -145,7 +149,8 @@ def run_gpu(case: Case, t, passes=("fwd", "dgrad", "wgrad"), dw_dtype=None, inv_
         out["dx"] = dx
     if "wgrad" in passes:
         fp32 = dw_dtype in (None, nc.NNCONV_F32)
-        dwt = Guarded(L.k * L.r * L.s * (L.c // L.groups), fp32=fp32, init=dw_old)
+        dwt = Guarded(L.k * L.r * L.s * (L.c // L.groups), fp32=fp32, init=dw_old,
+                      shift=dw_shift)
         ws, nb = workspace(d, nc.NNCONV_WGRAD)
         inv = (1.0 / case.loss_scale) if inv_scale is None else inv_scale
         nc.check(nc.nnconv_wgrad(d, x.data_ptr(), dy.data_ptr(), dwt.ptr(),

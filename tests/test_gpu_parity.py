@@ -162,6 +162,27 @@ def test_wgrad_accumulate_and_half_output():
     assert orc.rel_err(to_nchw(case, "dw", r["dw"]), ref) <= TOL[I.F16]
 
 
+@pytest.mark.parametrize("dw_dtype", ["f32", "f16"])
+def test_wgrad_unaligned_dw(dw_dtype):
+    """dw that is only element-aligned takes per-element stores; the bits
+    match the vector-store result (same summation order)."""
+    case = Case(L("z", 2, 64, 10, 9, 128, 3, 3, 1, 1), loss_scale=1024.0, dy_std=1e-3)
+    t = case.tensors()
+    dt = nc.NNCONV_F32 if dw_dtype == "f32" else nc.NNCONV_F16
+    rng = np.random.default_rng(5)
+    old = rng.standard_normal(128 * 9 * 64).astype(np.float32)
+    if dw_dtype == "f16":
+        old = I.to_bits(old, I.F16)
+    a = run_gpu(case, t, passes=("wgrad",), dw_dtype=dt, accumulate=1, dw_old=old)
+    b = run_gpu(case, t, passes=("wgrad",), dw_dtype=dt, accumulate=1, dw_old=old, dw_shift=1)
+    assert np.array_equal(a["dw_bits"], b["dw_bits"])
+    x, w, dy = nchw_f64(case, t)
+    oldf = old.astype(np.float64) if dw_dtype == "f32" else I.from_bits(old, I.F16)
+    ref = oracle_conv(case).wgrad(x, dy, 1.0 / 1024, beta=1,
+                                  dw_old=oldf.reshape(128, 3, 3, 64).transpose(0, 3, 1, 2))
+    assert orc.rel_err(to_nchw(case, "dw", b["dw"]), ref) <= (1e-5 if dw_dtype == "f32" else TOL[I.F16])
+
+
 def test_transforms_bit_exact():
     tt = torch()
     rng = np.random.default_rng(3)

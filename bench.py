@@ -50,6 +50,14 @@ def parse():
                          "(for profiling one shape; the reported value then covers only them)")
     ap.add_argument("--per-layer", default="",
                     help="write a per-layer / per-pass roofline table to this file")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before the steps, run one plain device copy of this many MiB "
+                         "(nnconv_pad_channels with no padding) as the reference dispatch "
+                         "for scaling FETCH_SIZE / WRITE_SIZE counters")
+    ap.add_argument("--summarize-profile", default="",
+                    help="no GPU work: summarise rocprofv3 CSV output under this directory "
+                         "(kernel trace and/or FETCH_SIZE / WRITE_SIZE counter runs of this "
+                         "script) and exit")
     return ap.parse_args()
 
 
@@ -151,6 +159,114 @@ def write_per_layer(path, layers, ev_steps, steps):
         f.write("total %.1f us, roofline %.1f us (%.1f%%)\n" % (tot, roof, 100 * roof / tot))
 
 
+# Sources that determine the forward launches (dispatch plans and kernels);
+# stored HBM-traffic counters are reported only while these are unchanged.
+FWD_SOURCES = ("api.hip", "common.hpp", "igemm_dma.hip", "igemm_v3.hip", "launch.hpp")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "igemm_fwd_traffic_resnet50_b256.txt")
+COPY_ROW_BYTES = 128    # calibration copy: rows of 64 fp16 channels
+
+
+def fwd_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in FWD_SOURCES:
+        with open(os.path.join(ROOT, "paper_2102_06725_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic():
+    """HBM bytes per forward launch from the committed FETCH_SIZE /
+    WRITE_SIZE counter summary, or None when it is missing or was taken on
+    other kernel sources."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("source_sha256") != fwd_source_hash():
+            return None
+        return float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def is_forward_launch(names, i):
+    """In this script's launch order (flag clear, then per layer: optional
+    stem channel padding, forward, backward-data kernels, backward-weight
+    kernel and its reduction) a forward launch is an implicit-GEMM dispatch
+    that follows a non-library dispatch, a split reduction or a padding
+    copy."""
+    n = names[i]
+    if "nnconv::" not in n or "igemm" not in n:
+        return False
+    if i == 0:
+        return True
+    prev = names[i - 1]
+    return "nnconv::" not in prev or "wgrad_reduce" in prev or "pad_channels" in prev
+
+
+def summarize_profile(args):
+    """Prints per-kernel totals and the forward-launch figures from rocprofv3
+    CSV output (kernel trace; FETCH_SIZE and WRITE_SIZE counter runs) of
+    `bench.py --calib-copy-mib M --steps K --warmup W`."""
+    import csv
+    import glob
+    import collections
+    nl = len(layers_for(args)[1])
+    skip = args.warmup * nl
+    out = []
+    for path in sorted(glob.glob(os.path.join(args.summarize_profile, "**", "*kernel_trace.csv"),
+                                 recursive=True)):
+        rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+        names = [r["Kernel_Name"] for r in rows]
+        dur = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows]
+        fam = collections.defaultdict(lambda: [0, 0])
+        for n, d in zip(names, dur):
+            key = n.split("(")[0].replace("void ", "") if "nnconv::" in n else "(torch / runtime)"
+            fam[key][0] += 1
+            fam[key][1] += d
+        tot = sum(v[1] for v in fam.values())
+        out.append("kernel trace: %s" % os.path.relpath(path, args.summarize_profile))
+        out.append("%-72s %7s %12s %10s %6s" % ("kernel", "calls", "total_us", "avg_us", "%"))
+        for k, v in sorted(fam.items(), key=lambda kv: -kv[1][1]):
+            out.append("%-72s %7d %12.1f %10.2f %6.2f" % (k[:72], v[0], v[1] / 1e3,
+                                                          v[1] / v[0] / 1e3, 100.0 * v[1] / tot))
+        fwd = [i for i in range(len(names)) if is_forward_launch(names, i)][skip:]
+        out.append("forward launches (after %d warm-up ones): %d, average %.2f us, total %.1f us"
+                   % (skip, len(fwd), sum(dur[i] for i in fwd) / max(1, len(fwd)) / 1e3,
+                      sum(dur[i] for i in fwd) / 1e3))
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        for path in sorted(glob.glob(os.path.join(args.summarize_profile, "**",
+                                                  "*counter_collection.csv"), recursive=True)):
+            rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+            if not rows:
+                continue
+            rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+            names = [r["Kernel_Name"] for r in rows]
+            kib = [float(r["Counter_Value"]) for r in rows]
+            line = "%s (%s):" % (counter, os.path.relpath(path, args.summarize_profile))
+            factor = None
+            if args.calib_copy_mib:
+                copy = [i for i, n in enumerate(names) if "pad_channels" in n][0]
+                factor = args.calib_copy_mib * 1024.0 / kib[copy]
+                line += " copy of %d MiB reads as %.1f KiB (factor %.4f);" % (
+                    args.calib_copy_mib, kib[copy], factor)
+            fwd = [i for i in range(len(names)) if is_forward_launch(names, i)][skip:]
+            per = sum(kib[i] for i in fwd) / max(1, len(fwd)) * 1024.0
+            line += " forward launches %d, %.1f MB per launch as counted" % (len(fwd), per / 1e6)
+            if factor is not None:
+                line += ", %.1f MB scaled" % (per * factor / 1e6)
+            out.append(line)
+            if factor is not None:
+                out.append("%s_bytes_per_launch: %.0f" % (
+                    "fetch" if counter == "FETCH_SIZE" else "write", per * factor))
+    out.append("source_sha256: %s" % fwd_source_hash())
+    print("\n".join(out))
+
+
 def cpu_baseline(args, wl):
     """The fp64 oracle as it stands, timed on this host's cores over a bounded
     sample: every distinct layer shape of the workload at batch 8, all its
@@ -205,6 +321,9 @@ def cpu_baseline(args, wl):
 
 def main():
     args = parse()
+    if args.summarize_profile:
+        summarize_profile(args)
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only (this build has no multi-GPU path); "
               "got --gpus %d" % args.gpus, file=sys.stderr)
@@ -225,6 +344,14 @@ def main():
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     flag = torch.zeros(1, dtype=torch.int32, device=dev)
     inv_s = 1.0 / wl.loss_scale
+    if args.calib_copy_mib:
+        rows = args.calib_copy_mib * 1024 * 1024 // COPY_ROW_BYTES
+        src = torch.ones((rows, COPY_ROW_BYTES // 2), device=dev, dtype=torch.float16)
+        dst = torch.empty_like(src)
+        nc.check(nc.nnconv_pad_channels(src.data_ptr(), dst.data_ptr(), rows,
+                                        COPY_ROW_BYTES // 2, COPY_ROW_BYTES // 2, sptr), "copy")
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
 
     def one_step(ev):
@@ -304,9 +431,12 @@ def main():
         fwd_avg_ms = pass_ms["fwd"] / pass_launch_units["fwd"]
         fwd_avg_flops = pass_flops["fwd"] / pass_launch_units["fwd"]
         ach = fwd_avg_flops / (fwd_avg_ms * 1e-3) / 1e12
-        roofline = {"kernel": "igemm_tn_kernel (forward launches)", "bound": "mfma",
-                    "achieved": ach, "peak": PEAK_F16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": ach / PEAK_F16_TFLOPS, "traffic": None,
+        traffic = stored_traffic() if args.workload == "sweep" and not args.layers and \
+            not args.batch and args.dtype == "f16" else None
+        roofline = {"kernel": "forward implicit GEMM (igemm_v3_kernel; igemm_dma_kernel for "
+                              "the stem), one launch per nnconv_fwd call",
+                    "bound": "mfma", "achieved": ach, "peak": PEAK_F16_TFLOPS,
+                    "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS, "traffic": traffic,
                     "avg_launch_us": fwd_avg_ms * 1e3,
                     "avg_flops_per_launch": fwd_avg_flops}
 

@@ -161,7 +161,7 @@ def write_per_layer(path, layers, ev_steps, steps):
 
 # Sources that determine the forward launches (dispatch plans and kernels);
 # stored HBM-traffic counters are reported only while these are unchanged.
-FWD_SOURCES = ("api.hip", "common.hpp", "igemm_dma.hip", "igemm_v3.hip", "launch.hpp")
+FWD_SOURCES = ("api.hip", "common.hpp", "igemm_c8.hip", "igemm_c64.hip", "launch.hpp")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "igemm_fwd_traffic_resnet50_b256.txt")
 COPY_ROW_BYTES = 128    # calibration copy: rows of 64 fp16 channels
 
@@ -433,7 +433,7 @@ def main():
         ach = fwd_avg_flops / (fwd_avg_ms * 1e-3) / 1e12
         traffic = stored_traffic() if args.workload == "sweep" and not args.layers and \
             not args.batch and args.dtype == "f16" else None
-        roofline = {"kernel": "forward implicit GEMM (igemm_v3_kernel; igemm_dma_kernel for "
+        roofline = {"kernel": "forward implicit GEMM (igemm_c64_kernel; igemm_c8_kernel for "
                               "the stem), one launch per nnconv_fwd call",
                     "bound": "mfma", "achieved": ach, "peak": PEAK_F16_TFLOPS,
                     "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS, "traffic": traffic,

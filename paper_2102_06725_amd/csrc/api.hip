@@ -212,22 +212,21 @@ TNParams tn_base() {
     return p;
 }
 
-TNConfig pick_tn(int64_t ncols) { return ncols <= 64 ? TN_256x64 : TN_128x128; }
+C8Config pick_c8(int64_t ncols) { return ncols <= 64 ? C8_256x64 : C8_128x128; }
 
 // Tile configuration from the output width and the reduction length
 // (taps x channels): reductions of at most SHORT_RED elements use the
 // single-stage tiles, several of which share a CU.
 constexpr int64_t SHORT_RED = 1024;
 
-V3Config pick_v3(int64_t ncols, int64_t red) {
+C64Config pick_c64(int64_t ncols, int64_t red) {
     if (red <= SHORT_RED) {
-        if (ncols <= 64) return V3S_256x64;
-        if (ncols <= 128) return V3S_256x128;
-        return V3S_128x256;
+        if (ncols <= 64) return C64S_128x64;
+        return C64S_128x128;
     }
-    if (ncols <= 64) return V3_256x64;
-    if (ncols <= 128) return V3_256x128;
-    return V3_256x256;
+    if (ncols <= 64) return C64_256x64;
+    if (ncols <= 128) return C64_256x128;
+    return C64_256x256;
 }
 
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
@@ -268,8 +267,8 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     p.taps.n = t;
     p.k_iters = (int32_t)((int64_t(t) * G.cg + 63) / 64);
     if (G.cg % 64 == 0)
-        return hip_status(launch_igemm_v3(G.dtype, pick_v3(G.kg, (int64_t)p.taps.n * G.cg), p, G.ph > 0 || G.pw > 0, st));
-    return hip_status(launch_igemm_dma(G.dtype, pick_tn(G.kg), p, st));
+        return hip_status(launch_igemm_c64(G.dtype, pick_c64(G.kg, (int64_t)p.taps.n * G.cg), p, G.ph > 0 || G.pw > 0, st));
+    return hip_status(launch_igemm_c8(G.dtype, pick_c8(G.kg), p, st));
 }
 
 // Backward-data as sigma_h * sigma_w independent implicit GEMMs, one per
@@ -325,9 +324,9 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             p.k_iters = (int32_t)((int64_t(t) * G.kg + 63) / 64);
             const bool pad = !(G.r == 1 && G.s == 1 && G.ph == 0 && G.pw == 0);
             if (G.kg % 64 == 0)
-                TRY_HIP(launch_igemm_v3(G.dtype, pick_v3(G.cg, (int64_t)t * G.kg), p, pad, st));
+                TRY_HIP(launch_igemm_c64(G.dtype, pick_c64(G.cg, (int64_t)t * G.kg), p, pad, st));
             else
-                TRY_HIP(launch_igemm_dma(G.dtype, pick_tn(G.cg), p, st));
+                TRY_HIP(launch_igemm_c8(G.dtype, pick_c8(G.cg), p, st));
         }
     }
     return NNCONV_OK;
@@ -356,7 +355,7 @@ nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *pa
     p.groups = (int32_t)G.g;
     p.splits = pl.splits;
     p.pix_per_split = pl.pix_per_split;
-    TRY_HIP(launch_wgrad_v2(G.dtype, pl.cfg, p, st));
+    TRY_HIP(launch_wgrad_splitk(G.dtype, pl.cfg, p, st));
     return NNCONV_OK;
 }
 

@@ -1,4 +1,4 @@
-// igemm_v3.hip -- large-tile implicit-GEMM convolution for the forward pass
+// igemm_c64.hip -- large-tile implicit-GEMM convolution for the forward pass
 // and each stride phase of the backward-data pass, for reductions whose
 // per-tap channel count is a multiple of 64 (every ResNet-50 layer but the
 // stem).
@@ -22,7 +22,7 @@
 
 namespace nnconv {
 
-namespace v3 {
+namespace c64 {
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -33,7 +33,12 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
 }
 
-__device__ __forceinline__ void barrier_lds() { asm volatile("s_barrier" ::: "memory"); }
+// Workgroup barrier for LDS hand-offs between waves: first wait until this
+// wave's own LDS reads and writes have completed (s_barrier alone does not),
+// so data written before the barrier is what other waves read after it.
+__device__ __forceinline__ void barrier_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // Buffer descriptor for bytes [base + shift, base + bytes) (gfx9 format).
 __device__ __forceinline__ i32x4 desc_at(const void *base, uint32_t bytes, uint32_t shift) {
@@ -72,12 +77,12 @@ __device__ __forceinline__ int slot(int r, int c) {
     return r * BKC + (c ^ swz<BKC>(r));
 }
 
-}  // namespace v3
+}  // namespace c64
 
 template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool PAD>
 __global__ __launch_bounds__(WM * WN * 64, (WM * WN == 4) ? ((BM * BN <= 128 * 128) ? 4 : 2) : 1)
-void igemm_v3_kernel(const TNParams P) {
-    using namespace v3;
+void igemm_c64_kernel(const TNParams P) {
+    using namespace c64;
     constexpr int NW = WM * WN;             // waves per workgroup
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int FM = WTM / 32, FN = WTN / 32;
@@ -289,17 +294,17 @@ void igemm_v3_kernel(const TNParams P) {
 }
 
 template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES>
-static hipError_t launch_v3_cfg(TNParams &p, bool pad, hipStream_t st) {
+static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
     p.tiles_m = (p.M + BM - 1) / BM;
     p.tiles_n = (p.ncols + BN - 1) / BN;
     const int64_t nb = (int64_t)p.tiles_m * p.tiles_n * p.groups;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (pad)
-        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, BKC, STAGES, true>),
+        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, true>),
                            dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     else
-        hipLaunchKernelGGL((igemm_v3_kernel<T, BM, BN, WM, WN, BKC, STAGES, false>),
+        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, false>),
                            dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
@@ -313,21 +318,20 @@ static hipError_t launch_v3_cfg(TNParams &p, bool pad, hipStream_t st) {
 // small LDS footprint lets 3-5 workgroups share a CU:
 //   128x128: 4 waves of 64x64 (32 KB);  128x64: 4 waves of 64x32 (24 KB)
 template <class T>
-static hipError_t launch_v3_t(V3Config cfg, TNParams &p, bool pad, hipStream_t st) {
+static hipError_t launch_c64_t(C64Config cfg, TNParams &p, bool pad, hipStream_t st) {
     switch (cfg) {
-        case V3_256x256: return launch_v3_cfg<T, 256, 256, 2, 4, 8, 2>(p, pad, st);
-        case V3_256x128: return launch_v3_cfg<T, 256, 128, 2, 2, 4, 3>(p, pad, st);
-        case V3S_128x256:
-        case V3S_256x128: return launch_v3_cfg<T, 128, 128, 2, 2, 8, 1>(p, pad, st);
-        case V3S_256x64: return launch_v3_cfg<T, 128, 64, 2, 2, 8, 1>(p, pad, st);
-        case V3_256x64:
-        default: return launch_v3_cfg<T, 256, 64, 4, 1, 4, 3>(p, pad, st);
+        case C64_256x256: return launch_c64_cfg<T, 256, 256, 2, 4, 8, 2>(p, pad, st);
+        case C64_256x128: return launch_c64_cfg<T, 256, 128, 2, 2, 4, 3>(p, pad, st);
+        case C64S_128x128: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 1>(p, pad, st);
+        case C64S_128x64: return launch_c64_cfg<T, 128, 64, 2, 2, 8, 1>(p, pad, st);
+        case C64_256x64:
+        default: return launch_c64_cfg<T, 256, 64, 4, 1, 4, 3>(p, pad, st);
     }
 }
 
-hipError_t launch_igemm_v3(int dtype, V3Config cfg, TNParams &p, bool pad, hipStream_t st) {
-    if (dtype == Half::id) return launch_v3_t<Half>(cfg, p, pad, st);
-    return launch_v3_t<BFloat>(cfg, p, pad, st);
+hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hipStream_t st) {
+    if (dtype == Half::id) return launch_c64_t<Half>(cfg, p, pad, st);
+    return launch_c64_t<BFloat>(cfg, p, pad, st);
 }
 
 }  // namespace nnconv

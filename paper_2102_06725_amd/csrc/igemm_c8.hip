@@ -1,10 +1,13 @@
-// igemm_dma.hip -- implicit-GEMM convolution (forward pass and each stride
-// phase of the backward-data pass) with a multi-stage global -> LDS pipeline
-// built on gfx950's direct-to-LDS buffer loads.
+// igemm_c8.hip -- implicit-GEMM convolution (forward pass and each stride
+// phase of the backward-data pass) for any per-tap channel count that is a
+// multiple of 8 (the stem after padding 3 -> 8 channels, small-C layers),
+// with a multi-stage global -> LDS pipeline built on gfx950's direct-to-LDS
+// buffer loads.
 //
-// Same GEMM view as igemm_tn.hip (rows = output pixels gathered through the
-// tap table, columns = output channels, reduction = (tap, channel)), but:
-//   - each k-slice is 32 reduction elements (4 x 16-byte chunks per row);
+// GEMM view: rows = output pixels gathered through the tap table, columns =
+// output channels, reduction = (tap, channel) with channels fastest:
+//   - each k-slice is 32 reduction elements (4 x 16-byte chunks per row),
+//     which may span several taps;
 //   - operand tiles go straight from HBM/L2 into LDS (no register staging),
 //     STAGES slices deep, so STAGES-1 slices of loads are in flight while
 //     the matrix cores work on the current one;
@@ -27,9 +30,14 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
 }
 
-// Workgroup barrier that also orders LDS accesses in the compiler's view
+// Workgroup barrier for LDS hand-offs between waves: first wait until this
+// wave's own LDS reads and writes have completed (s_barrier alone does not),
+// so data written before the barrier is what other waves read after it.  The
+// memory clobber also keeps the compiler from moving LDS accesses across it
 // (the direct-to-LDS loads are invisible to its dependence tracking).
-__device__ __forceinline__ void barrier_lds() { asm volatile("s_barrier" ::: "memory"); }
+__device__ __forceinline__ void barrier_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -74,7 +82,7 @@ __device__ __forceinline__ int slot_of(int r, int c) {
 }
 
 template <class T, int BM, int BN, int BKC, int STAGES, bool ALIGNED>
-__global__ __launch_bounds__(256, 2) void igemm_dma_kernel(const TNParams P) {
+__global__ __launch_bounds__(256, 2) void igemm_c8_kernel(const TNParams P) {
     constexpr int WM = 2, WN = 2;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int FM = WTM / 32, FN = WTN / 32;
@@ -270,7 +278,7 @@ __global__ __launch_bounds__(256, 2) void igemm_dma_kernel(const TNParams P) {
 }
 
 template <class T, int BM, int BN, int BKC, int STAGES>
-static hipError_t launch_dma_cfg(TNParams &p, hipStream_t st) {
+static hipError_t launch_c8_cfg(TNParams &p, hipStream_t st) {
     p.tiles_m = (p.M + BM - 1) / BM;
     p.tiles_n = (p.ncols + BN - 1) / BN;
     const int64_t nb = (int64_t)p.tiles_m * p.tiles_n * p.groups;
@@ -279,27 +287,27 @@ static hipError_t launch_dma_cfg(TNParams &p, hipStream_t st) {
     // k_iters counts BKC*8-element slices here
     p.k_iters = (int32_t)(((int64_t)p.taps.n * p.cr + BKC * 8 - 1) / (BKC * 8));
     if (p.cr % (BKC * 8) == 0)
-        hipLaunchKernelGGL((igemm_dma_kernel<T, BM, BN, BKC, STAGES, true>), dim3((uint32_t)nb),
+        hipLaunchKernelGGL((igemm_c8_kernel<T, BM, BN, BKC, STAGES, true>), dim3((uint32_t)nb),
                            dim3(256), 0, st, p);
     else
-        hipLaunchKernelGGL((igemm_dma_kernel<T, BM, BN, BKC, STAGES, false>), dim3((uint32_t)nb),
+        hipLaunchKernelGGL((igemm_c8_kernel<T, BM, BN, BKC, STAGES, false>), dim3((uint32_t)nb),
                            dim3(256), 0, st, p);
     return hipGetLastError();
 }
 
 template <class T>
-static hipError_t launch_dma_t(TNConfig cfg, TNParams &p, hipStream_t st) {
+static hipError_t launch_c8_t(C8Config cfg, TNParams &p, hipStream_t st) {
     switch (cfg) {
-        case TN_256x64: return launch_dma_cfg<T, 256, 64, 4, 4>(p, st);
-        case TN_256x128: return launch_dma_cfg<T, 256, 128, 4, 3>(p, st);
-        case TN_128x128:
-        default: return launch_dma_cfg<T, 128, 128, 4, 4>(p, st);
+        case C8_256x64: return launch_c8_cfg<T, 256, 64, 4, 4>(p, st);
+        case C8_256x128: return launch_c8_cfg<T, 256, 128, 4, 3>(p, st);
+        case C8_128x128:
+        default: return launch_c8_cfg<T, 128, 128, 4, 4>(p, st);
     }
 }
 
-hipError_t launch_igemm_dma(int dtype, TNConfig cfg, TNParams &p, hipStream_t st) {
-    if (dtype == Half::id) return launch_dma_t<Half>(cfg, p, st);
-    return launch_dma_t<BFloat>(cfg, p, st);
+hipError_t launch_igemm_c8(int dtype, C8Config cfg, TNParams &p, hipStream_t st) {
+    if (dtype == Half::id) return launch_c8_t<Half>(cfg, p, st);
+    return launch_c8_t<BFloat>(cfg, p, st);
 }
 
 }  // namespace nnconv

@@ -57,19 +57,19 @@ struct TNParams {
     TapTable taps;
 };
 
-enum TNConfig { TN_128x128 = 0, TN_256x64 = 1, TN_256x128 = 2 };
+// Any cr (a multiple of 8): the reduction is cut into slices of 32 elements
+// built from 8-channel chunks of consecutive taps (recomputes k_iters for
+// its own slice depth).
+enum C8Config { C8_128x128 = 0, C8_256x64 = 1, C8_256x128 = 2 };
+hipError_t launch_igemm_c8(int dtype, C8Config cfg, TNParams &p, hipStream_t st);
 
-hipError_t launch_igemm_tn(int dtype, TNConfig cfg, TNParams &p, hipStream_t st);
-// Same GEMM with the multi-stage direct-to-LDS pipeline (recomputes k_iters
-// for its own slice depth).
-hipError_t launch_igemm_dma(int dtype, TNConfig cfg, TNParams &p, hipStream_t st);
-
-// Large-tile variant for cr % 64 == 0 (k_iters is derived from the taps).
-// pad: some (row, tap) pairs fall outside the A image and must read zeros.
-enum V3Config { V3_256x256 = 0, V3_256x128 = 1, V3_256x64 = 2,
-                // single-stage variants for reductions of a few 64-element slices
-                V3S_128x256 = 3, V3S_256x128 = 4, V3S_256x64 = 5 };
-hipError_t launch_igemm_v3(int dtype, V3Config cfg, TNParams &p, bool pad, hipStream_t st);
+// cr % 64 == 0: 64-channel slices of one tap (k_iters is derived from the
+// taps).  pad: some (row, tap) pairs fall outside the A image and must read
+// zeros.
+enum C64Config { C64_256x256 = 0, C64_256x128 = 1, C64_256x64 = 2,
+                 // single-stage tiles for reductions of a few 64-element slices
+                 C64S_128x128 = 3, C64S_128x64 = 4 };
+hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hipStream_t st);
 
 // Backward-weight split-K partial sums:
 //   ws[split][k][j] = sum over pixels of this split of dy[pix, k] * xcol[pix, j]
@@ -92,10 +92,8 @@ struct WGParams {
 
 enum WGConfig { WG_128x128 = 0, WG_64x128 = 1, WG_256x128 = 2, WG_128x256 = 3, WG_256x256 = 4 };
 
+// Pixel ranges of pix_per_split (a multiple of 32) pixels each.
 hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);
-// Same partial sums with direct-to-LDS pixel-major staging and transposing
-// LDS reads (pix_per_split must be a multiple of 32).
-hipError_t launch_wgrad_v2(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);
 
 // dw[e'] = (accumulate ? dw[e'] : 0) + inv_scale * sum_{s < splits} ws[s][e]
 // over e < count = K * R*S*Cg; e' = e for [K][R][S][Cg] output, or the

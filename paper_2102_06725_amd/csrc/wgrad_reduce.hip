@@ -1,218 +1,12 @@
-// wgrad.hip -- backward-weight pass: split-K implicit GEMM on the gfx950
-// matrix cores, then a fixed-order reduction with the loss-scale epilogue.
-//
-// GEMM view:  dW[k, j] = sum_pix dy[pix, k] * xcol[pix, j],  j = (r, s, c)
-// The reduction runs over batch pixels, which is the strided dimension of
-// both channel-last operands.  Each thread loads PPT consecutive pixels x 8
-// consecutive channels (16-byte, coalesced along channels), transposes the
-// block in registers and writes it to LDS as rows of pixels, so the MFMA
-// fragment reads are the same 16-byte row reads as in the forward kernel.
-// Pixels are split into `splits` ranges; each range writes an fp32 partial
-// tile to the workspace.
+// wgrad_reduce.hip -- second half of the backward-weight pass: the sum of
+// the split-K fp32 partials in a fixed order, the loss-scale step
+// (multiply by the inverse loss scale, optional accumulation into the old
+// gradient), conversion to the output type and the non-finite check.
 #include <type_traits>
 
 #include "launch.hpp"
 
 namespace nnconv {
-
-// Write a PPT-pixel x 8-channel register block transposed into LDS rows
-// row0..row0+7 (one row per channel) at pixel offset pix0 of a 64-pixel row.
-template <int PPT>
-__device__ __forceinline__ void store_transposed(uint32_t *lds, int row0, int pix0,
-                                                 const u32x4 (&v)[PPT]) {
-    static_assert(PPT == 2 || PPT == 4, "2 or 4 pixels per thread");
-#pragma unroll
-    for (int e8 = 0; e8 < 8; ++e8) {
-        uint32_t wds[PPT / 2];
-#pragma unroll
-        for (int a = 0; a < PPT / 2; ++a) {
-            const uint32_t lo = v[2 * a][e8 >> 1];
-            const uint32_t hi = v[2 * a + 1][e8 >> 1];
-            wds[a] = (e8 & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-        }
-        const int r = row0 + e8;
-        const int pc = (pix0 >> 3) ^ swz(r);
-        const int addr = (r * 8 + pc) * 4 + ((pix0 & 7) >> 1);
-        if constexpr (PPT == 4) {
-            u32x2 w2;
-            w2[0] = wds[0];
-            w2[1] = wds[1];
-            *(u32x2 *)(lds + addr) = w2;
-        } else {
-            lds[addr] = wds[0];
-        }
-    }
-}
-
-template <class T, int BMK, int BNJ, int WM, int WN>
-__global__ __launch_bounds__(256, 2) void wgrad_splitk_kernel(const WGParams P) {
-    constexpr int CH = 8;                   // 16-byte chunks per 64-pixel LDS row
-    constexpr int KCH = BMK / 8;            // channel chunks of the dy tile
-    constexpr int JCH = BNJ / 8;            // column chunks of the x tile
-    constexpr int PPTK = 64 * KCH / 256;    // pixels per thread, dy tile
-    constexpr int PPTJ = 64 * JCH / 256;    // pixels per thread, x tile
-    constexpr int WTM = BMK / WM, WTN = BNJ / WN;
-    constexpr int FM = WTM / 32, FN = WTN / 32;
-    static_assert(WM * WN == 4, "4 waves per workgroup");
-
-    __shared__ u32x4 lds[2][(BMK + BNJ) * CH];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave % WM, wn = wave / WM;
-
-    // tile: groups x splits x m-tiles x n-tiles, n fastest
-    const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
-    const int per_split = P.tiles_m * P.tiles_n;
-    const int per_g = per_split * P.splits;
-    const int g = (int)lid / per_g;
-    int rem = (int)lid - g * per_g;
-    const int split = rem / per_split;
-    rem -= split * per_split;
-    const int tm = rem / P.tiles_n;
-    const int tn = rem - tm * P.tiles_n;
-    const int k0 = tm * BMK, j0 = tn * BNJ;
-
-    const int pix_begin = split * P.pix_per_split;
-    const int pix_end = min(P.npq, pix_begin + P.pix_per_split);
-    const int k_iters = pix_end > pix_begin ? (pix_end - pix_begin + 63) / 64 : 0;
-
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(P.x, P.x_bytes);
-    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(P.dy, P.dy_bytes);
-
-    // dy staging role: channel chunk kc, pixel group pgk
-    const int kc = tid % KCH, pgk = tid / KCH;
-    const bool k_ok = k0 + kc * 8 < P.kg;
-    const int dy_ch = g * P.kg + k0 + kc * 8;
-    // x staging role: column chunk jc (fixed tap and channel), pixel group pgj
-    const int jc = tid % JCH, pgj = tid / JCH;
-    const int jcol = j0 + jc * 8;
-    const bool j_ok = jcol < P.rscg;
-    int tap_dh = 0, tap_dw = 0, x_ch = 0;
-    if (j_ok) {
-        const int tap = (int)fdiv((uint32_t)jcol, P.div_cg);
-        const int c0 = jcol - tap * P.cg;
-        const int r = (int)fdiv((uint32_t)tap, P.div_s);
-        const int ss = tap - r * (int)P.div_s.d;
-        tap_dh = r * P.dh - P.ph;
-        tap_dw = ss * P.dw - P.pw;
-        x_ch = g * P.cg + c0;
-    }
-
-    u32x4 sk[PPTK], sj[PPTJ];
-    auto gload = [&](int kt) {
-        const int base = pix_begin + kt * 64;
-#pragma unroll
-        for (int e = 0; e < PPTK; ++e) {
-            const int pix = base + pgk * PPTK + e;
-            const bool ok = k_ok && pix < pix_end;
-            const uint32_t off = (uint32_t)(pix * P.k + dy_ch) * 2u;
-            sk[e] = load16(rdy, ok ? off : OOB_OFFSET);
-        }
-#pragma unroll
-        for (int e = 0; e < PPTJ; ++e) {
-            const int pix = base + pgj * PPTJ + e;
-            bool ok = j_ok && pix < pix_end;
-            const int pc = ok ? pix : 0;
-            const int n = (int)fdiv((uint32_t)pc, P.div_pq);
-            const int rm = pc - n * (P.p * P.q);
-            const int pp = (int)fdiv((uint32_t)rm, P.div_q);
-            const int qq = rm - pp * P.q;
-            const int h = pp * P.sh + tap_dh;
-            const int w = qq * P.sw + tap_dw;
-            ok = ok && (unsigned)h < (unsigned)P.h && (unsigned)w < (unsigned)P.w;
-            const int off = (((n * P.h + h) * P.w + w) * P.c + x_ch) * 2;
-            sj[e] = load16(rx, ok ? (uint32_t)off : OOB_OFFSET);
-        }
-    };
-    auto lstore = [&](int buf) {
-        uint32_t *base = (uint32_t *)&lds[buf][0];
-        store_transposed<PPTK>(base, kc * 8, pgk * PPTK, sk);
-        store_transposed<PPTJ>(base + BMK * CH * 4, jc * 8, pgj * PPTJ, sj);
-    };
-
-    f32x16 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
-
-    if (k_iters > 0) {
-        gload(0);
-        lstore(0);
-    }
-    __syncthreads();
-
-    const int l32 = lane & 31;
-    const int khalf = lane >> 5;
-    for (int kt = 0; kt < k_iters; ++kt) {
-        const int buf = kt & 1;
-        const bool more = kt + 1 < k_iters;
-        if (more) gload(kt + 1);
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const int kq = 2 * ks + khalf;
-            u32x4 fa[FM], fb[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int r = wm * WTM + i * 32 + l32;
-                fa[i] = lds[buf][r * CH + (kq ^ swz(r))];
-            }
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int r = wn * WTN + j * 32 + l32;
-                fb[j] = lds[buf][(BMK + r) * CH + (kq ^ swz(r))];
-            }
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<T>(fa[i], fb[j], acc[i][j]);
-        }
-        if (more) lstore(buf ^ 1);
-        __syncthreads();
-    }
-
-    // lane holds column l32 of each 32-column block and rows 8*e + 4*khalf + {0..3}
-    const int K = P.kg * P.groups;
-    float *ws = P.ws + (int64_t)split * K * P.rscg;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int col = j0 + wn * WTN + j * 32 + l32;
-        if (col >= P.rscg) continue;
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int row = k0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
-                if (row < P.kg) ws[(int64_t)(g * P.kg + row) * P.rscg + col] = acc[i][j][v];
-            }
-        }
-    }
-}
-
-template <class T, int BMK, int BNJ, int WM, int WN>
-static hipError_t launch_wg(WGParams &p, hipStream_t st) {
-    p.tiles_m = (p.kg + BMK - 1) / BMK;
-    p.tiles_n = (p.rscg + BNJ - 1) / BNJ;
-    const int64_t nb = (int64_t)p.tiles_m * p.tiles_n * p.splits * p.groups;
-    if (nb <= 0) return hipSuccess;
-    if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((wgrad_splitk_kernel<T, BMK, BNJ, WM, WN>), dim3((uint32_t)nb), dim3(256),
-                       0, st, p);
-    return hipGetLastError();
-}
-
-template <class T>
-static hipError_t launch_wg_t(WGConfig cfg, WGParams &p, hipStream_t st) {
-    if (cfg == WG_64x128) return launch_wg<T, 64, 128, 2, 2>(p, st);
-    return launch_wg<T, 128, 128, 2, 2>(p, st);
-}
-
-hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st) {
-    if (dtype == Half::id) return launch_wg_t<Half>(cfg, p, st);
-    return launch_wg_t<BFloat>(cfg, p, st);
-}
 
 // ---------------------------------------------------------------------------
 // reduction over splits + loss-scale epilogue

@@ -1,4 +1,4 @@
-// wgrad_v2.hip -- backward-weight split-K implicit GEMM with direct-to-LDS
+// wgrad_splitk.hip -- backward-weight split-K implicit GEMM with direct-to-LDS
 // staging and gfx950 transposing LDS reads.
 //
 // GEMM view:  dW[k, j] = sum_pix dy[pix, k] * xcol[pix, j],  j = (r, s, c).
@@ -19,7 +19,7 @@
 
 namespace nnconv {
 
-namespace wg2 {
+namespace wgs {
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -32,7 +32,12 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
 }
 
-__device__ __forceinline__ void barrier_lds() { asm volatile("s_barrier" ::: "memory"); }
+// Workgroup barrier for LDS hand-offs between waves: first wait until this
+// wave's own LDS reads and writes have completed (s_barrier alone does not),
+// so data written before the barrier is what other waves read after it.
+__device__ __forceinline__ void barrier_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 __device__ __forceinline__ i32x4 desc_of(const void *base, uint32_t bytes) {
     const uint64_t a = (uint64_t)base;
@@ -69,11 +74,11 @@ __device__ __forceinline__ uint32_t tile_off(int p, int co) {
     return (uint32_t)(p * ROWB + (((byte >> 6) ^ seg_swz<ROWB>(p)) << 6) + (byte & 63));
 }
 
-}  // namespace wg2
+}  // namespace wgs
 
 template <class T, int BM, int BN, int WM, int WN, int BKP, int STAGES>
-__global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 1024) ? 1 : 2) void wgrad_v2_kernel(const WGParams P) {
-    using namespace wg2;
+__global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 1024) ? 1 : 2) void wgrad_splitk_kernel(const WGParams P) {
+    using namespace wgs;
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int FM = WTM / 32, FN = WTN / 32;
@@ -257,13 +262,13 @@ __global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 
 }
 
 template <class T, int BM, int BN, int WM, int WN, int BKP, int STAGES>
-static hipError_t launch_wg2(WGParams &p, hipStream_t st) {
+static hipError_t launch_wgs(WGParams &p, hipStream_t st) {
     p.tiles_m = (p.kg + BM - 1) / BM;
     p.tiles_n = (p.rscg + BN - 1) / BN;
     const int64_t nb = (int64_t)p.tiles_m * p.tiles_n * p.splits * p.groups;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((wgrad_v2_kernel<T, BM, BN, WM, WN, BKP, STAGES>), dim3((uint32_t)nb),
+    hipLaunchKernelGGL((wgrad_splitk_kernel<T, BM, BN, WM, WN, BKP, STAGES>), dim3((uint32_t)nb),
                        dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
@@ -275,19 +280,19 @@ static hipError_t launch_wg2(WGParams &p, hipStream_t st) {
 //   128x256: 4 waves of 64x128, 32-pixel slices, 3 stages (72 KB)
 //   256x256: 8 waves of 128x64, 32-pixel slices, 3 stages (96 KB)
 template <class T>
-static hipError_t launch_wg2_t(WGConfig cfg, WGParams &p, hipStream_t st) {
+static hipError_t launch_wgs_t(WGConfig cfg, WGParams &p, hipStream_t st) {
     switch (cfg) {
-        case WG_64x128: return launch_wg2<T, 64, 128, 2, 2, 32, 3>(p, st);
-        case WG_256x128: return launch_wg2<T, 256, 128, 2, 2, 32, 3>(p, st);
-        case WG_128x256: return launch_wg2<T, 128, 256, 2, 2, 32, 3>(p, st);
-        case WG_256x256: return launch_wg2<T, 256, 256, 2, 4, 32, 3>(p, st);
-        default: return launch_wg2<T, 128, 128, 2, 2, 32, 3>(p, st);
+        case WG_64x128: return launch_wgs<T, 64, 128, 2, 2, 32, 3>(p, st);
+        case WG_256x128: return launch_wgs<T, 256, 128, 2, 2, 32, 3>(p, st);
+        case WG_128x256: return launch_wgs<T, 128, 256, 2, 2, 32, 3>(p, st);
+        case WG_256x256: return launch_wgs<T, 256, 256, 2, 4, 32, 3>(p, st);
+        default: return launch_wgs<T, 128, 128, 2, 2, 32, 3>(p, st);
     }
 }
 
-hipError_t launch_wgrad_v2(int dtype, WGConfig cfg, WGParams &p, hipStream_t st) {
-    if (dtype == Half::id) return launch_wg2_t<Half>(cfg, p, st);
-    return launch_wg2_t<BFloat>(cfg, p, st);
+hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st) {
+    if (dtype == Half::id) return launch_wgs_t<Half>(cfg, p, st);
+    return launch_wgs_t<BFloat>(cfg, p, st);
 }
 
 }  // namespace nnconv

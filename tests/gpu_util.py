@@ -92,18 +92,21 @@ class Case:
 
 def nchw_f64(case: Case, t):
     """Operands as float64 in the oracle's [N][C][H][W] / [K][Cg][R][S] form,
-    restricted to the logical channels (the stem's pad channels dropped)."""
+    restricted to the logical channels (the stem's pad channels dropped).
+    The 16-bit patterns are rearranged first, then converted."""
     L = case.layer
-    x = I.from_bits(t["x"], case.dtype)
-    w = I.from_bits(t["w"], case.dtype)
-    dy = I.from_bits(t["dy"], case.dtype)
-    if case.layout == "nhwc":
-        x = x.transpose(0, 3, 1, 2)
-        w = w.transpose(0, 3, 1, 2)
-        dy = dy.transpose(0, 3, 1, 2)
     cl = L.c_alg
-    return np.ascontiguousarray(x[:, :cl]), np.ascontiguousarray(w[:, :cl // L.groups]), \
-        np.ascontiguousarray(dy)
+    x, w, dy = t["x"], t["w"], t["dy"]
+    if case.layout == "nhwc":
+        x = x[..., :cl].transpose(0, 3, 1, 2)
+        w = w[..., :cl // L.groups].transpose(0, 3, 1, 2)
+        dy = dy.transpose(0, 3, 1, 2)
+    else:
+        x = x[:, :cl]
+        w = w[:, :cl // L.groups]
+    return (I.from_bits(np.ascontiguousarray(x), case.dtype),
+            I.from_bits(np.ascontiguousarray(w), case.dtype),
+            I.from_bits(np.ascontiguousarray(dy), case.dtype))
 
 
 def oracle_conv(case: Case):

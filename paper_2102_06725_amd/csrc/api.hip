@@ -76,23 +76,28 @@ struct WgPlan {
     int32_t splits, pix_per_split;
 };
 
+// Backward-weight tile and workgroup target, from measurements on the
+// ResNet-50 layers at batch 256: 128x128 tiles with about 512 workgroups are
+// within a few per cent of the best choice on every layer with Kg > 64; with
+// Kg <= 64 a 64-row tile and more pixel splits (1024 workgroups) win.
 WGConfig pick_wg(int64_t kg, int64_t rscg) {
-    if (kg <= 64) return WG_64x128;
-    if (kg <= 128) return rscg >= 256 ? WG_128x256 : WG_128x128;
-    return rscg >= 256 ? WG_256x256 : WG_256x128;
+    (void)rscg;
+    return kg <= 64 ? WG_64x128 : WG_128x128;
 }
+
+int64_t wg_target_blocks(WGConfig cfg) { return cfg == WG_64x128 ? 1024 : 512; }
 
 WgPlan plan_wgrad_fast(const Geom &G) {
     WgPlan pl;
     const int64_t rscg = G.r * G.s * G.cg;
     pl.cfg = pick_wg(G.kg, rscg);
-    static const int64_t tile_m[] = {128, 64, 256, 128, 256};
-    static const int64_t tile_n[] = {128, 128, 128, 256, 256};
+    static const int64_t tile_m[] = {128, 64};
+    static const int64_t tile_n[] = {128, 128};
     const int64_t bmk = tile_m[pl.cfg], bnj = tile_n[pl.cfg];
     const int64_t tiles = G.g * ((G.kg + bmk - 1) / bmk) * ((rscg + bnj - 1) / bnj);
     const int64_t npq = G.n * G.p * G.q;
     const int64_t iters = (npq + 63) / 64;  // 64-pixel units
-    const int64_t target = 512;
+    const int64_t target = wg_target_blocks(pl.cfg);
     int64_t splits = (target + tiles - 1) / tiles;
     int64_t max_splits = iters / 4;  // at least 256 pixels per split
     if (max_splits < 1) max_splits = 1;
@@ -214,19 +219,26 @@ TNParams tn_base() {
 
 C8Config pick_c8(int64_t ncols) { return ncols <= 64 ? C8_256x64 : C8_128x128; }
 
-// Tile configuration from the output width and the reduction length
-// (taps x channels): reductions of at most SHORT_RED elements use the
-// single-stage tiles, several of which share a CU.
-constexpr int64_t SHORT_RED = 1024;
+// Tile configuration for the 64-channel-slice kernel, from measurements on
+// the ResNet-50 layers at batch 256 (m = GEMM rows, ncols = output channels
+// per group, red = reduction length):
+//   - the per-CU load path (about 64 bytes per clock) keeps the matrix
+//     cores busy only with 256x256 tiles (128 flop per staged byte); they
+//     win on long reductions once there are enough tiles to give most CUs
+//     one (3x3 layers on 14x14 with 256 output channels, GEMM-sized
+//     problems);
+//   - otherwise the single-stage 128-row tiles, 3-5 per CU, hide each
+//     other's load latency best; very long reductions prefer the pipelined
+//     128x128 tile.
+constexpr int64_t MIN_BIG_TILES = 160;
+constexpr int64_t BIG_RED = 2048;
+constexpr int64_t LONG_RED = 4096;
 
-C64Config pick_c64(int64_t ncols, int64_t red) {
-    if (red <= SHORT_RED) {
-        if (ncols <= 64) return C64S_128x64;
-        return C64S_128x128;
-    }
-    if (ncols <= 64) return C64_256x64;
-    if (ncols <= 128) return C64_256x128;
-    return C64_256x256;
+C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
+    if (ncols <= 64) return C64S_128x64;
+    const int64_t big_tiles = ((m + 255) / 256) * ((ncols + 255) / 256);
+    if (ncols >= 256 && red >= BIG_RED && big_tiles >= MIN_BIG_TILES) return C64_256x256;
+    return red >= LONG_RED ? C64_128x128 : C64S_128x128;
 }
 
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
@@ -267,7 +279,8 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     p.taps.n = t;
     p.k_iters = (int32_t)((int64_t(t) * G.cg + 63) / 64);
     if (G.cg % 64 == 0)
-        return hip_status(launch_igemm_c64(G.dtype, pick_c64(G.kg, (int64_t)p.taps.n * G.cg), p, G.ph > 0 || G.pw > 0, st));
+        return hip_status(launch_igemm_c64(G.dtype, pick_c64(p.M, G.kg, (int64_t)p.taps.n * G.cg), p,
+                                           G.ph > 0 || G.pw > 0, st));
     return hip_status(launch_igemm_c8(G.dtype, pick_c8(G.kg), p, st));
 }
 
@@ -324,7 +337,7 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             p.k_iters = (int32_t)((int64_t(t) * G.kg + 63) / 64);
             const bool pad = !(G.r == 1 && G.s == 1 && G.ph == 0 && G.pw == 0);
             if (G.kg % 64 == 0)
-                TRY_HIP(launch_igemm_c64(G.dtype, pick_c64(G.cg, (int64_t)t * G.kg), p, pad, st));
+                TRY_HIP(launch_igemm_c64(G.dtype, pick_c64(p.M, G.cg, (int64_t)t * G.kg), p, pad, st));
             else
                 TRY_HIP(launch_igemm_c8(G.dtype, pick_c8(G.cg), p, st));
         }

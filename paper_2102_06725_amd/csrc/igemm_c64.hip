@@ -309,23 +309,21 @@ static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
     return hipGetLastError();
 }
 
-// Configurations (LDS per workgroup in parentheses; <= 80 KB lets two
-// workgroups share a CU):
+// Configurations (LDS per workgroup in parentheses):
 //   256x256: 8 waves of 128x64, 64-element slices, 2 stages (128 KB)
-//   256x128: 4 waves of 128x64, 32-element slices, 3 stages (72 KB)
-//   256x64 : 4 waves of  64x64, 32-element slices, 3 stages (60 KB)
-// Short reductions (a few 64-element slices) use single-stage tiles whose
-// small LDS footprint lets 3-5 workgroups share a CU:
+//   128x128: 4 waves of 64x64, 64-element slices, 2 stages (64 KB; two
+//            workgroups per CU)
+// Single-stage tiles, whose small LDS footprint lets 3-5 workgroups share a
+// CU and cover each other's load latency:
 //   128x128: 4 waves of 64x64 (32 KB);  128x64: 4 waves of 64x32 (24 KB)
 template <class T>
 static hipError_t launch_c64_t(C64Config cfg, TNParams &p, bool pad, hipStream_t st) {
     switch (cfg) {
         case C64_256x256: return launch_c64_cfg<T, 256, 256, 2, 4, 8, 2>(p, pad, st);
-        case C64_256x128: return launch_c64_cfg<T, 256, 128, 2, 2, 4, 3>(p, pad, st);
-        case C64S_128x128: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 1>(p, pad, st);
+        case C64_128x128: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 2>(p, pad, st);
         case C64S_128x64: return launch_c64_cfg<T, 128, 64, 2, 2, 8, 1>(p, pad, st);
-        case C64_256x64:
-        default: return launch_c64_cfg<T, 256, 64, 4, 1, 4, 3>(p, pad, st);
+        case C64S_128x128:
+        default: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 1>(p, pad, st);
     }
 }
 

@@ -66,9 +66,10 @@ hipError_t launch_igemm_c8(int dtype, C8Config cfg, TNParams &p, hipStream_t st)
 // cr % 64 == 0: 64-channel slices of one tap (k_iters is derived from the
 // taps).  pad: some (row, tap) pairs fall outside the A image and must read
 // zeros.
-enum C64Config { C64_256x256 = 0, C64_256x128 = 1, C64_256x64 = 2,
-                 // single-stage tiles for reductions of a few 64-element slices
-                 C64S_128x128 = 3, C64S_128x64 = 4 };
+enum C64Config { C64_256x256 = 0,   // 8 waves, 64-element slices, 2 stages
+                 C64_128x128 = 1,   // 4 waves, 64-element slices, 2 stages
+                 C64S_128x128 = 2,  // single stage (several workgroups per CU)
+                 C64S_128x64 = 3 };
 hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hipStream_t st);
 
 // Backward-weight split-K partial sums:
@@ -90,7 +91,7 @@ struct WGParams {
     int32_t tiles_m, tiles_n;   // filled by the launcher
 };
 
-enum WGConfig { WG_128x128 = 0, WG_64x128 = 1, WG_256x128 = 2, WG_128x256 = 3, WG_256x256 = 4 };
+enum WGConfig { WG_128x128 = 0, WG_64x128 = 1 };
 
 // Pixel ranges of pix_per_split (a multiple of 32) pixels each.
 hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);

@@ -77,22 +77,26 @@ struct WgPlan {
 };
 
 // Backward-weight tile and workgroup target, from measurements on the
-// ResNet-50 layers at batch 256: 128x128 tiles with about 512 workgroups are
-// within a few per cent of the best choice on every layer with Kg > 64; with
-// Kg <= 64 a 64-row tile and more pixel splits (1024 workgroups) win.
+// ResNet-50 layers at batch 256: 256x256 tiles and about 256 workgroups
+// (long pixel ranges, few partial tiles to write and reduce) when both GEMM
+// sides are at least 256 wide; 64-row tiles and more pixel splits (1024
+// workgroups) when Kg <= 64; otherwise 128x128 tiles and 512 workgroups.
 WGConfig pick_wg(int64_t kg, int64_t rscg) {
-    (void)rscg;
-    return kg <= 64 ? WG_64x128 : WG_128x128;
+    if (kg <= 64) return WG_64x128;
+    if (kg >= 256 && rscg >= 256 && rscg < 4096) return WG_256x256;
+    return WG_128x128;
 }
 
-int64_t wg_target_blocks(WGConfig cfg) { return cfg == WG_64x128 ? 1024 : 512; }
+int64_t wg_target_blocks(WGConfig cfg) {
+    return cfg == WG_64x128 ? 1024 : cfg == WG_256x256 ? 256 : 512;
+}
 
 WgPlan plan_wgrad_fast(const Geom &G) {
     WgPlan pl;
     const int64_t rscg = G.r * G.s * G.cg;
     pl.cfg = pick_wg(G.kg, rscg);
-    static const int64_t tile_m[] = {128, 64};
-    static const int64_t tile_n[] = {128, 128};
+    static const int64_t tile_m[] = {128, 64, 256};
+    static const int64_t tile_n[] = {128, 128, 256};
     const int64_t bmk = tile_m[pl.cfg], bnj = tile_n[pl.cfg];
     const int64_t tiles = G.g * ((G.kg + bmk - 1) / bmk) * ((rscg + bnj - 1) / bnj);
     const int64_t npq = G.n * G.p * G.q;

@@ -276,9 +276,11 @@ static hipError_t launch_wgs(WGParams &p, hipStream_t st) {
 // Configurations (LDS per workgroup):
 //    64x128: 4 waves of 32x64, 32-pixel slices, 3 stages (36 KB)
 //   128x128: 4 waves of 64x64, 32-pixel slices, 3 stages (48 KB)
+//   256x256: 8 waves of 128x64, 32-pixel slices, 3 stages (96 KB)
 template <class T>
 static hipError_t launch_wgs_t(WGConfig cfg, WGParams &p, hipStream_t st) {
     if (cfg == WG_64x128) return launch_wgs<T, 64, 128, 2, 2, 32, 3>(p, st);
+    if (cfg == WG_256x256) return launch_wgs<T, 256, 256, 2, 4, 32, 3>(p, st);
     return launch_wgs<T, 128, 128, 2, 2, 32, 3>(p, st);
 }
 

@@ -245,8 +245,40 @@ C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
     return red >= LONG_RED ? C64_128x128 : C64S_128x128;
 }
 
+// Compute units of the current device (the persistent kernels launch one
+// workgroup per CU).
+int device_cus() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
+        cus = 256;
+    return cus;
+}
+
+// 8-channel pixels into 64 channels with the stem's filter: the patch kernel.
+bool stem_shape(const Geom &G) {
+    return G.cg == 8 && G.g == 1 && G.k == 64 && G.dh == 1 && G.dw == 1 &&
+           stem_fwd_supported((int)G.r, (int)G.s, (int)G.sh, (int)G.sw);
+}
+
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
                        hipStream_t st) {
+    if (stem_shape(G)) {
+        StemParams sp;
+        sp.x = x;
+        sp.x_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+        sp.wt = w;
+        sp.wt_bytes = (uint32_t)(G.k * G.r * G.s * G.cg * 2);
+        sp.y = y;
+        sp.y_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
+        sp.n = (int32_t)G.n; sp.h = (int32_t)G.h; sp.w = (int32_t)G.w;
+        sp.p = (int32_t)G.p; sp.q = (int32_t)G.q;
+        sp.r = (int32_t)G.r; sp.s = (int32_t)G.s; sp.sh = (int32_t)G.sh; sp.sw = (int32_t)G.sw;
+        sp.ph = (int32_t)G.ph; sp.pw = (int32_t)G.pw;
+        sp.alpha = alpha;
+        return hip_status(launch_stem_fwd(G.dtype, sp, device_cus(), st));
+    }
     TNParams p = tn_base();
     p.a = x;
     p.a_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);

@@ -72,6 +72,24 @@ enum C64Config { C64_256x256 = 0,   // 8 waves, 64-element slices, 2 stages
                  C64S_128x64 = 3 };
 hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hipStream_t st);
 
+// Forward pass for 8-channel (16-byte) channel-last pixels, 64 output
+// channels, groups 1, dilation 1 and a compiled filter size / stride (the
+// stem: 7x7, stride 2).  x [n][h][w][8], wt [64][r][s][8], y [n][p][q][64].
+struct StemParams {
+    const void *x;
+    uint32_t x_bytes;
+    const void *wt;
+    uint32_t wt_bytes;
+    void *y;
+    uint32_t y_bytes;
+    int32_t n, h, w, p, q;
+    int32_t r, s, sh, sw, ph, pw;
+    float alpha;
+};
+bool stem_fwd_supported(int r, int s, int sh, int sw);
+// cus: workgroups to launch at most (one per CU; the kernel loops over tiles)
+hipError_t launch_stem_fwd(int dtype, const StemParams &p, int cus, hipStream_t st);
+
 // Backward-weight split-K partial sums:
 //   ws[split][k][j] = sum over pixels of this split of dy[pix, k] * xcol[pix, j]
 // with j = (r*S + s)*Cg + c (the [K][R][S][Cg] order) and channel-last x, dy.

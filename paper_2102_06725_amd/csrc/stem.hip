@@ -1,0 +1,250 @@
+// stem.hip -- forward convolution for 8-channel (16-byte) pixels and 64
+// output channels with a fixed filter size and stride (the ResNet stem after
+// padding its 3 input channels to 8): a persistent implicit GEMM that stages
+// an input patch and the whole filter in LDS instead of gathering an im2col
+// row per (pixel, tap) from L2.
+//
+// Output tiles are 16 x 16 pixels of one image.  The input patch of a tile
+// ((16-1)*SH + R rows by (16-1)*SW + S columns of 16-byte pixels) arrives in
+// LDS with buffer_load ... lds, columns split by phase (column mod SW), so
+// the 16 consecutive output pixels of a fragment read 16 consecutive 16-byte
+// entries for any tap.  The filter, [64][taps][8] with the tap count padded to
+// an even number (the pad tap is zero) and the row stride made odd in 16-byte
+// units, stays in LDS for the workgroup's lifetime.  While one tile is
+// computed, the next tile's patch is already being loaded into the other
+// patch buffer.
+//
+// GEMM view per tile: rows = 256 output pixels, columns = 64 output channels,
+// reduction = taps x 8 channels; one v_mfma_f32_32x32x16 k-step covers two
+// taps, so an operand fragment is one 16-byte LDS read per lane.
+#include "launch.hpp"
+
+namespace nnconv {
+
+namespace stem {
+
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int TH = 16, TW = 16;  // output tile
+constexpr int K = 64;            // output channels
+
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
+}
+
+// Barrier for LDS hand-offs between waves: the wave's own LDS accesses are
+// complete before it signals (s_barrier alone does not wait for them).
+__device__ __forceinline__ void barrier_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+__device__ __forceinline__ i32x4 desc_of(const void *base, uint32_t bytes) {
+    const uint64_t a = (uint64_t)base;
+    i32x4 d;
+    d[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)a);
+    d[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(a >> 32) & 0xFFFFu));
+    d[2] = __builtin_amdgcn_readfirstlane((int32_t)bytes);
+    d[3] = 0x00020000;
+    return d;
+}
+
+// buffer_load_dwordx4 ... lds: lane i's 16 bytes land at lds_addr + 16*i;
+// offsets past the descriptor's range deliver zeros.
+__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 desc) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(desc)
+        : "memory");
+}
+
+template <int R, int S, int SH, int SW>
+struct Geo {
+    static constexpr int TAPS = R * S;
+    static constexpr int TAPS2 = (TAPS + 1) & ~1;           // even, >= TAPS
+    static constexpr int WROW = TAPS2 | 1;                  // odd row stride (16-byte units)
+    static constexpr int W_ENT = K * WROW;                  // filter entries
+    static constexpr int PR = (TH - 1) * SH + R;            // patch rows
+    static constexpr int PC = (TW - 1) * SW + S;            // patch columns
+    static constexpr int PHC = (PC + SW - 1) / SW;          // columns per phase
+    static constexpr int PROW = SW * PHC;                   // entries per patch row
+    static constexpr int P_ENT = ((PR * PROW + 63) / 64) * 64;  // whole 1-KB loads
+    static constexpr int C_ENT = TH * TW * K / 8;           // output tile, 16-byte chunks
+    static constexpr int LDS_ENT = W_ENT + 2 * P_ENT + C_ENT;
+};
+
+}  // namespace stem
+
+template <class T, int R, int S, int SH, int SW>
+__global__ __launch_bounds__(256, 1) void stem_fwd_kernel(const StemParams P) {
+    using namespace stem;
+    using G = Geo<R, S, SH, SW>;
+    static_assert(G::LDS_ENT * 16 <= 160 * 1024, "LDS budget");
+    __shared__ u32x4 lds[G::LDS_ENT];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void *)&lds[0];
+    const uint32_t wbase = lds0;
+    const uint32_t pbase0 = lds0 + G::W_ENT * 16;
+
+    const i32x4 dx = desc_of(P.x, P.x_bytes);
+    const i32x4 dw = desc_of(P.wt, P.wt_bytes);
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(P.y, P.y_bytes);
+
+    const int tiles_q = (P.q + TW - 1) / TW, tiles_p = (P.p + TH - 1) / TH;
+    const int per_img = tiles_p * tiles_q;
+    const int total = P.n * per_img;
+
+    // filter: entry e = k * WROW + t holds w[k][t][0..7]; taps >= R*S are 0
+    for (int e0 = wave * 64; e0 < G::W_ENT; e0 += 4 * 64) {
+        const int e = e0 + lane;
+        const int k = e / G::WROW, t = e - k * G::WROW;
+        const uint32_t off = (e < G::W_ENT && t < G::TAPS) ? (uint32_t)(k * G::TAPS + t) * 16u
+                                                             : OOB_OFFSET;
+        dma16(wbase + (uint32_t)e0 * 16u, off, dw);
+    }
+
+    // patch of tile `tile` into buffer b
+    auto load_patch = [&](int tile, int b) {
+        const int n = tile / per_img;
+        const int rem = tile - n * per_img;
+        const int tp = rem / tiles_q, tq = rem - tp * tiles_q;
+        const int ih0 = tp * TH * SH - P.ph, iw0 = tq * TW * SW - P.pw;
+        const uint32_t pb = pbase0 + (uint32_t)(b * G::P_ENT) * 16u;
+#pragma unroll
+        for (int j = 0; j < (G::P_ENT / 64 + 3) / 4; ++j) {
+            const int e0 = (j * 4 + wave) * 64;
+            if (e0 < G::P_ENT) {
+                const int e = e0 + lane;
+                const int pr = e / G::PROW;
+                const int rem2 = e - pr * G::PROW;
+                const int ph = rem2 / G::PHC;
+                const int pc = (rem2 - ph * G::PHC) * SW + ph;
+                const int ih = ih0 + pr, iw = iw0 + pc;
+                const bool ok = pr < G::PR && pc < G::PC && (unsigned)ih < (unsigned)P.h &&
+                                (unsigned)iw < (unsigned)P.w;
+                const uint32_t off = ok ? (uint32_t)((n * P.h + ih) * P.w + iw) * 16u : OOB_OFFSET;
+                dma16(pb + (uint32_t)e0 * 16u, off, dx);
+            }
+        }
+    };
+
+    // wave w owns tile pixels 64w .. 64w+63 (rows 4w .. 4w+3); fragment i
+    // covers rows 4w+2i, 4w+2i+1; lane l: row + (l&31)/16, column l&15
+    const int l32 = lane & 31, khalf = lane >> 5;
+    int a_row[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) a_row[i] = 4 * wave + 2 * i + (l32 >> 4);
+    const int a_col = l32 & 15;
+    // entry of (output pixel, tap t) within a patch buffer
+    auto a_entry = [&](int i, int t) -> int {
+        const int r = t / S, s = t - (t / S) * S;
+        return (a_row[i] * SH + r) * G::PROW + (s % SW) * G::PHC + a_col + s / SW;
+    };
+
+    int tile = blockIdx.x;
+    if (tile < total) load_patch(tile, 0);
+    wait_vmcnt<0>();
+    barrier_lds();
+
+    int buf = 0;
+    for (; tile < total; tile += gridDim.x) {
+        const int next = tile + gridDim.x;
+        if (next < total) load_patch(next, buf ^ 1);
+
+        f32x16 acc[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+        const u32x4 *pt = &lds[G::W_ENT + buf * G::P_ENT];
+        const u32x4 *wt = &lds[0];
+#pragma unroll
+        for (int ks = 0; ks < G::TAPS2 / 2; ++ks) {
+            const int t = 2 * ks + khalf;
+            u32x4 fa[2], fb[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                fa[i] = t < G::TAPS ? pt[a_entry(i, t < G::TAPS ? t : 0)] : wt[G::TAPS];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) fb[j] = wt[(j * 32 + l32) * G::WROW + t];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<T>(fb[j], fa[i], acc[i][j]);
+        }
+
+        // epilogue: C tile [256 px][8 chunks of 8 channels] in LDS (chunk
+        // swizzled by pixel), then one 16-byte store per lane
+        {
+            char *cl = (char *)&lds[G::W_ENT + 2 * G::P_ENT];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int px = 64 * wave + 32 * i + l32;
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        // lane holds channels 32j + 8e + 4*khalf + {0..3} of pixel px
+                        const int c = 4 * j + e;
+                        u32x2 pk;
+                        pk[0] = to16<T>(acc[i][j][4 * e + 0] * P.alpha) |
+                                (to16<T>(acc[i][j][4 * e + 1] * P.alpha) << 16);
+                        pk[1] = to16<T>(acc[i][j][4 * e + 2] * P.alpha) |
+                                (to16<T>(acc[i][j][4 * e + 3] * P.alpha) << 16);
+                        *(u32x2 *)(cl + (px * 8 + (c ^ (px & 7))) * 16 + khalf * 8) = pk;
+                    }
+                }
+            }
+        }
+        barrier_lds();  // C tile complete; every wave is done with patch `buf`
+        {
+            const int n = tile / (tiles_p * tiles_q);
+            const int rem = tile - n * tiles_p * tiles_q;
+            const int tp = rem / tiles_q, tq = rem - tp * tiles_q;
+            // always the same number of store instructions per thread (pixels
+            // outside the output are discarded by the range check), so the
+            // vmcnt wait below counts exactly these stores
+#pragma unroll
+            for (int it = 0; it < TH * TW * 8 / 256; ++it) {
+                const int idx = it * 256 + tid;
+                const int px = idx >> 3, c = idx & 7;
+                const int oh = tp * TH + (px >> 4), ow = tq * TW + (px & 15);
+                const uint32_t o = (oh < P.p && ow < P.q)
+                                       ? (uint32_t)(((n * P.p + oh) * P.q + ow) * K + c * 8) * 2u
+                                       : OOB_OFFSET;
+                const u32x4 v = lds[G::W_ENT + 2 * G::P_ENT + px * 8 + (c ^ (px & 7))];
+                __builtin_amdgcn_raw_buffer_store_b128(v, ry, o, 0, 0);
+            }
+        }
+        // the next patch has landed (its loads precede this tile's stores)
+        wait_vmcnt<TH * TW * 8 / 256>();
+        barrier_lds();  // next patch visible; C tile free for reuse
+        buf ^= 1;
+    }
+    wait_vmcnt<0>();
+}
+
+template <class T, int R, int S, int SH, int SW>
+static hipError_t launch_stem_t(const StemParams &p, int cus, hipStream_t st) {
+    const int64_t tiles =
+        (int64_t)p.n * ((p.p + stem::TH - 1) / stem::TH) * ((p.q + stem::TW - 1) / stem::TW);
+    if (tiles <= 0) return hipSuccess;
+    const int grid = (int)(tiles < cus ? tiles : cus);
+    hipLaunchKernelGGL((stem_fwd_kernel<T, R, S, SH, SW>), dim3(grid), dim3(256), 0, st, p);
+    return hipGetLastError();
+}
+
+bool stem_fwd_supported(int r, int s, int sh, int sw) { return r == 7 && s == 7 && sh == 2 && sw == 2; }
+
+hipError_t launch_stem_fwd(int dtype, const StemParams &p, int cus, hipStream_t st) {
+    if (!stem_fwd_supported(p.r, p.s, p.sh, p.sw)) return hipErrorInvalidValue;
+    if (dtype == Half::id) return launch_stem_t<Half, 7, 7, 2, 2>(p, cus, st);
+    return launch_stem_t<BFloat, 7, 7, 2, 2>(p, cus, st);
+}
+
+}  // namespace nnconv

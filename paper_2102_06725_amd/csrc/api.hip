@@ -71,7 +71,17 @@ bool fast_shape(const Geom &G) {
 // planning: workspace regions and split counts (pure functions of the shape)
 // ---------------------------------------------------------------------------
 
+// 8-channel pixels into 64 channels with the stem's filter: the patch kernel.
+bool stem_shape(const Geom &G) {
+    return G.cg == 8 && G.g == 1 && G.k == 64 && G.dh == 1 && G.dw == 1 &&
+           stem_fwd_supported((int)G.r, (int)G.s, (int)G.sh, (int)G.sw);
+}
+
+// Stem backward-weight: persistent workgroups (one split-K partial each).
+constexpr int64_t STEM_WG_SPLITS = 256;
+
 struct WgPlan {
+    bool stem;  // patch kernel (stem_shape)
     WGConfig cfg;
     int32_t splits, pix_per_split;
 };
@@ -93,6 +103,14 @@ int64_t wg_target_blocks(WGConfig cfg) {
 
 WgPlan plan_wgrad_fast(const Geom &G) {
     WgPlan pl;
+    pl.stem = stem_shape(G);
+    if (pl.stem) {
+        const int64_t tiles = G.n * ((G.p + 15) / 16) * ((G.q + 15) / 16);
+        pl.cfg = WG_128x128;
+        pl.splits = (int32_t)(tiles < STEM_WG_SPLITS ? tiles : STEM_WG_SPLITS);
+        pl.pix_per_split = 0;
+        return pl;
+    }
     const int64_t rscg = G.r * G.s * G.cg;
     pl.cfg = pick_wg(G.kg, rscg);
     static const int64_t tile_m[] = {128, 64, 256};
@@ -256,12 +274,6 @@ int device_cus() {
     return cus;
 }
 
-// 8-channel pixels into 64 channels with the stem's filter: the patch kernel.
-bool stem_shape(const Geom &G) {
-    return G.cg == 8 && G.g == 1 && G.k == 64 && G.dh == 1 && G.dw == 1 &&
-           stem_fwd_supported((int)G.r, (int)G.s, (int)G.sh, (int)G.sw);
-}
-
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
                        hipStream_t st) {
     if (stem_shape(G)) {
@@ -384,6 +396,22 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
 nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *part,
                          hipStream_t st) {
     const WgPlan pl = plan_wgrad_fast(G);
+    if (pl.stem) {
+        StemParams sp;
+        sp.x = x;
+        sp.x_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+        sp.wt = nullptr;
+        sp.wt_bytes = 0;
+        sp.y = const_cast<void *>(dy);
+        sp.y_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
+        sp.n = (int32_t)G.n; sp.h = (int32_t)G.h; sp.w = (int32_t)G.w;
+        sp.p = (int32_t)G.p; sp.q = (int32_t)G.q;
+        sp.r = (int32_t)G.r; sp.s = (int32_t)G.s; sp.sh = (int32_t)G.sh; sp.sw = (int32_t)G.sw;
+        sp.ph = (int32_t)G.ph; sp.pw = (int32_t)G.pw;
+        sp.alpha = 1.0f;
+        TRY_HIP(launch_stem_wgrad(G.dtype, sp, part, pl.splits, st));
+        return NNCONV_OK;
+    }
     WGParams p;
     memset(&p, 0, sizeof(p));
     p.x = x;

@@ -89,6 +89,10 @@ struct StemParams {
 bool stem_fwd_supported(int r, int s, int sh, int sw);
 // cus: workgroups to launch at most (one per CU; the kernel loops over tiles)
 hipError_t launch_stem_fwd(int dtype, const StemParams &p, int cus, hipStream_t st);
+// Backward-weight partials for the same shapes: y holds dy; splits
+// workgroups each write part[split][64][r*s*8] (no loss-scale step).
+hipError_t launch_stem_wgrad(int dtype, const StemParams &p, float *part, int splits,
+                             hipStream_t st);
 
 // Backward-weight split-K partial sums:
 //   ws[split][k][j] = sum over pixels of this split of dy[pix, k] * xcol[pix, j]

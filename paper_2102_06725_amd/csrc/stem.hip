@@ -229,6 +229,189 @@ __global__ __launch_bounds__(256, 1) void stem_fwd_kernel(const StemParams P) {
     wait_vmcnt<0>();
 }
 
+// Backward-weight for the same shapes: each persistent workgroup sums
+//   part[k][t*8 + c] = sum over its pixels of dy[pix][k] * patch(pix, t)[c]
+// over the output tiles blockIdx.x, blockIdx.x + gridDim.x, ... into fp32
+// registers and writes one split-K partial (reduced in a fixed order by the
+// split reduction).  Per tile the 16x16 dy block ([pixel][64 channels],
+// 128-byte rows, 64-byte segments swizzled) and the input patch come in by
+// buffer_load ... lds, double-buffered.  The matrix-core operands need 8
+// consecutive pixels per lane; the transposing LDS read supplies them: for dy
+// a 4-pixel x 16-channel block per 16 lanes, for the patch 4 pixels x
+// (2 taps x 8 channels), since consecutive output pixels of a tile row are
+// consecutive patch entries.  Patch entries outside the receptive field of
+// the tile's in-range output pixels are loaded as zeros, so pixels past the
+// output edge (whose dy rows are zero) add exact zeros.
+namespace stem {
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// byte offset of (pixel row p, 16-bit channel co) in a 128-byte-row dy tile:
+// 64-byte segment s of row p lives at segment s ^ ((p >> 1) & 1)
+__device__ __forceinline__ uint32_t dy_off(int p, int co) {
+    const int byte = co * 2;
+    return (uint32_t)(p * 128 + ((((byte >> 6) ^ ((p >> 1) & 1))) << 6) + (byte & 63));
+}
+
+__device__ __forceinline__ u32x4 pack_tr(s16x4 v0, s16x4 v1) {
+    u32x4 r;
+    r[0] = (uint32_t)(uint16_t)v0[0] | ((uint32_t)(uint16_t)v0[1] << 16);
+    r[1] = (uint32_t)(uint16_t)v0[2] | ((uint32_t)(uint16_t)v0[3] << 16);
+    r[2] = (uint32_t)(uint16_t)v1[0] | ((uint32_t)(uint16_t)v1[1] << 16);
+    r[3] = (uint32_t)(uint16_t)v1[2] | ((uint32_t)(uint16_t)v1[3] << 16);
+    return r;
+}
+}  // namespace stem
+
+template <class T, int R, int S, int SH, int SW>
+__global__ __launch_bounds__(256, 1) void stem_wgrad_kernel(const StemParams P, float *part) {
+    using namespace stem;
+    using G = Geo<R, S, SH, SW>;
+    constexpr int CB = (G::TAPS + 3) / 4;            // 32-column blocks (4 taps each)
+    constexpr int DY_ENT = TH * TW * K / 8;          // dy tile, 16-byte entries
+    constexpr int BUF_ENT = G::P_ENT + DY_ENT;
+    constexpr int LDS_ENT = 2 * BUF_ENT + 1;          // + one zero entry
+    static_assert(LDS_ENT * 16 <= 160 * 1024, "LDS budget");
+    __shared__ u32x4 lds[LDS_ENT];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void *)&lds[0];
+    const i32x4 dx = desc_of(P.x, P.x_bytes);
+    const i32x4 ddy = desc_of(P.y, P.y_bytes);
+
+    const int tiles_q = (P.q + TW - 1) / TW, tiles_p = (P.p + TH - 1) / TH;
+    const int per_img = tiles_p * tiles_q;
+    const int total = P.n * per_img;
+
+    if (tid == 0) lds[2 * BUF_ENT] = u32x4{};
+
+    auto load_tile = [&](int tile, int b) {
+        const int n = tile / per_img;
+        const int rem = tile - n * per_img;
+        const int tp = rem / tiles_q, tq = rem - tp * tiles_q;
+        const int vh = min(TH, P.p - tp * TH), vw = min(TW, P.q - tq * TW);
+        const int prv = (vh - 1) * SH + R, pcv = (vw - 1) * SW + S;  // receptive field
+        const int ih0 = tp * TH * SH - P.ph, iw0 = tq * TW * SW - P.pw;
+        const uint32_t pb = lds0 + (uint32_t)(b * BUF_ENT) * 16u;
+#pragma unroll
+        for (int j = 0; j < (G::P_ENT / 64 + 3) / 4; ++j) {
+            const int e0 = (j * 4 + wave) * 64;
+            if (e0 < G::P_ENT) {
+                const int e = e0 + lane;
+                const int pr = e / G::PROW;
+                const int rem2 = e - pr * G::PROW;
+                const int ph = rem2 / G::PHC;
+                const int pc = (rem2 - ph * G::PHC) * SW + ph;
+                const int ih = ih0 + pr, iw = iw0 + pc;
+                const bool ok = pr < prv && pc < pcv && (unsigned)ih < (unsigned)P.h &&
+                                (unsigned)iw < (unsigned)P.w;
+                const uint32_t off = ok ? (uint32_t)((n * P.h + ih) * P.w + iw) * 16u : OOB_OFFSET;
+                dma16(pb + (uint32_t)e0 * 16u, off, dx);
+            }
+        }
+        // dy: entry e = physical chunk of pixel row p = e / 8; physical 64-byte
+        // segment (e & 7) >> 2 holds logical segment ^ ((p >> 1) & 1)
+        const uint32_t db = pb + (uint32_t)G::P_ENT * 16u;
+#pragma unroll
+        for (int j = 0; j < DY_ENT / 256; ++j) {
+            const int e = (j * 4 + wave) * 64 + lane;
+            const int p = e >> 3, q8 = e & 7;
+            const int lchunk = (((q8 >> 2) ^ ((p >> 1) & 1)) << 2) | (q8 & 3);
+            const int oh = tp * TH + (p >> 4), ow = tq * TW + (p & 15);
+            const uint32_t off = (oh < P.p && ow < P.q)
+                                     ? (uint32_t)(((n * P.p + oh) * P.q + ow) * K + lchunk * 8) * 2u
+                                     : OOB_OFFSET;
+            dma16(db + (uint32_t)((j * 4 + wave) * 64) * 16u, off, ddy);
+        }
+    };
+
+    // wave w: column blocks w, w+4, w+8, ... (both 32-row halves of K)
+    constexpr int MAXC = (CB + 3) / 4;
+    f32x16 acc[MAXC][2];
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[c][i] = f32x16{};
+
+    const int li = lane & 15, g = lane >> 4;
+    const int pix_half = 8 * (g >> 1);   // pixel offset of this lane's 8 k-slots
+    // dy fragment source (transposing read): pixel row pix_half + 4*rd + li/4,
+    // channels 16*(g&1) + 4*(li&3) + 32*rowblock
+    // patch fragment source: pixel pix_half + 4*rd + li/4, tap offset
+    // ((li&3) >> 1), 8-byte half (li&1)
+    const int src_px = pix_half + (li >> 2);
+    const int a_ch = 16 * (g & 1) + 4 * (li & 3);
+    const int b_tap = 2 * (g & 1) + ((li & 3) >> 1);
+    const int b_half = li & 1;
+    const uint32_t zero_addr = lds0 + (uint32_t)(2 * BUF_ENT) * 16u;
+
+    int tile = blockIdx.x;
+    if (tile < total) load_tile(tile, 0);
+    wait_vmcnt<0>();
+    barrier_lds();
+
+    int buf = 0;
+    for (; tile < total; tile += gridDim.x) {
+        const int next = tile + gridDim.x;
+        if (next < total) load_tile(next, buf ^ 1);
+        const uint32_t pb = lds0 + (uint32_t)(buf * BUF_ENT) * 16u;
+        const uint32_t db = pb + (uint32_t)G::P_ENT * 16u;
+#pragma unroll 2
+        for (int row = 0; row < TH; ++row) {   // one k16 step = one tile row of 16 pixels
+            u32x4 fa[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int p0 = row * TW + src_px;
+                const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4 *)(uintptr_t)(db + dy_off(p0, 32 * i + a_ch)));
+                const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4 *)(uintptr_t)(db + dy_off(p0 + 4, 32 * i + a_ch)));
+                fa[i] = pack_tr(v0, v1);
+            }
+#pragma unroll
+            for (int c = 0; c < MAXC; ++c) {
+                const int cb = wave + 4 * c;
+                if (cb < CB) {
+                    const int t = cb * 4 + b_tap;
+                    uint32_t a0 = zero_addr, a1 = zero_addr;
+                    if (t < G::TAPS) {
+                        const int r = t / S, s = t - (t / S) * S;
+                        const int e = (row * SH + r) * G::PROW + (s % SW) * G::PHC + src_px + s / SW;
+                        a0 = pb + (uint32_t)e * 16u + b_half * 8;
+                        a1 = a0 + 4 * 16;
+                    }
+                    const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(uintptr_t)a0);
+                    const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(uintptr_t)a1);
+                    const u32x4 fb = pack_tr(v0, v1);
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) acc[c][i] = mfma32<T>(fa[i], fb, acc[c][i]);
+                }
+            }
+        }
+        wait_vmcnt<0>();
+        barrier_lds();
+        buf ^= 1;
+    }
+
+    // partial [64][TAPS*8]: lane holds column l&31 of each block, rows
+    // 8*(v/4) + 4*(l/32) + v%4 of each 32-row half
+    const int ncol = G::TAPS * 8;
+    float *dst = part + (int64_t)blockIdx.x * K * ncol;
+    const int l32 = lane & 31, kh = lane >> 5;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        const int cb = wave + 4 * c;
+        const int col = cb * 32 + l32;
+        if (cb < CB && col < ncol) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    dst[(32 * i + 8 * (v >> 2) + 4 * kh + (v & 3)) * ncol + col] = acc[c][i][v];
+        }
+    }
+}
+
 template <class T, int R, int S, int SH, int SW>
 static hipError_t launch_stem_t(const StemParams &p, int cus, hipStream_t st) {
     const int64_t tiles =
@@ -240,6 +423,18 @@ static hipError_t launch_stem_t(const StemParams &p, int cus, hipStream_t st) {
 }
 
 bool stem_fwd_supported(int r, int s, int sh, int sw) { return r == 7 && s == 7 && sh == 2 && sw == 2; }
+
+hipError_t launch_stem_wgrad(int dtype, const StemParams &p, float *part, int splits,
+                             hipStream_t st) {
+    if (!stem_fwd_supported(p.r, p.s, p.sh, p.sw) || splits < 1) return hipErrorInvalidValue;
+    if (dtype == Half::id)
+        hipLaunchKernelGGL((stem_wgrad_kernel<Half, 7, 7, 2, 2>), dim3(splits), dim3(256), 0, st, p,
+                           part);
+    else
+        hipLaunchKernelGGL((stem_wgrad_kernel<BFloat, 7, 7, 2, 2>), dim3(splits), dim3(256), 0, st,
+                           p, part);
+    return hipGetLastError();
+}
 
 hipError_t launch_stem_fwd(int dtype, const StemParams &p, int cus, hipStream_t st) {
     if (!stem_fwd_supported(p.r, p.s, p.sh, p.sw)) return hipErrorInvalidValue;

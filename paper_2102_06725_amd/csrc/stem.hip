@@ -356,7 +356,7 @@ __global__ __launch_bounds__(256, 1) void stem_wgrad_kernel(const StemParams P, 
         if (next < total) load_tile(next, buf ^ 1);
         const uint32_t pb = lds0 + (uint32_t)(buf * BUF_ENT) * 16u;
         const uint32_t db = pb + (uint32_t)G::P_ENT * 16u;
-#pragma unroll 2
+#pragma unroll
         for (int row = 0; row < TH; ++row) {   // one k16 step = one tile row of 16 pixels
             u32x4 fa[2];
 #pragma unroll

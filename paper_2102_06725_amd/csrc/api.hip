@@ -274,6 +274,22 @@ int device_cus() {
     return cus;
 }
 
+TNPhase phase_of(int64_t m, int64_t mi, int64_t mj, int64_t oi_add, int64_t oj_add, int tap_start,
+                 int tap_count) {
+    TNPhase f;
+    memset(&f, 0, sizeof(f));
+    f.M = (int32_t)m;
+    f.mi = (int32_t)mi;
+    f.mj = (int32_t)mj;
+    f.div_mj = make_fastdiv((uint32_t)(mj > 0 ? mj : 1));
+    f.div_mi = make_fastdiv((uint32_t)(mi > 0 ? mi : 1));
+    f.oi_add = (int32_t)oi_add;
+    f.oj_add = (int32_t)oj_add;
+    f.tap_start = tap_start;
+    f.tap_count = tap_count;
+    return f;
+}
+
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
                        hipStream_t st) {
     if (stem_shape(G)) {
@@ -326,9 +342,12 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
         }
     p.taps.n = t;
     p.k_iters = (int32_t)((int64_t(t) * G.cg + 63) / 64);
-    if (G.cg % 64 == 0)
-        return hip_status(launch_igemm_c64(G.dtype, pick_c64(p.M, G.kg, (int64_t)p.taps.n * G.cg), p,
+    if (G.cg % 64 == 0) {
+        p.nphase = 1;
+        p.ph[0] = phase_of(p.M, p.mi, p.mj, 0, 0, 0, t);
+        return hip_status(launch_igemm_c64(G.dtype, pick_c64(p.M, G.kg, (int64_t)t * G.cg), p,
                                            G.ph > 0 || G.pw > 0, st));
+    }
     return hip_status(launch_igemm_c8(G.dtype, pick_c8(G.kg), p, st));
 }
 
@@ -337,57 +356,96 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
 // sees the same set of contributing taps.  wt is [g][R][S][Cg][Kg].
 nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx, float alpha,
                          hipStream_t st) {
+    TNParams base = tn_base();
+    base.a = dy;
+    base.a_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
+    base.b = wt;
+    base.b_bytes = (uint32_t)(G.k * G.r * G.s * G.cg * 2);
+    base.out = dx;
+    base.o_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+    base.a_h = (int32_t)G.p; base.a_w = (int32_t)G.q; base.a_c = (int32_t)G.k;
+    base.a_cg_ofs = (int32_t)G.kg;
+    base.ai_mul = 1; base.ai_add = 0; base.aj_mul = 1; base.aj_add = 0;
+    base.cr = (int32_t)G.kg;
+    base.div_crv = make_fastdiv((uint32_t)(G.kg / 8));
+    base.ncols = (int32_t)G.cg;
+    base.b_ld = (int32_t)G.kg;
+    base.b_g_ofs = (int32_t)(G.r * G.s * G.cg * G.kg);
+    base.o_h = (int32_t)G.h; base.o_w = (int32_t)G.w; base.o_c = (int32_t)G.c;
+    base.o_cg_ofs = (int32_t)G.cg;
+    base.oi_mul = (int32_t)G.sh;
+    base.oj_mul = (int32_t)G.sw;
+    base.alpha = alpha;
+    base.groups = (int32_t)G.g;
+    const bool pad = !(G.r == 1 && G.s == 1 && G.ph == 0 && G.pw == 0);
+    // taps of output phase (phh, phw), appended to p.taps; returns their count
+    auto add_phase_taps = [&](TNParams &p, int64_t phh, int64_t phw) {
+        int t = 0;
+        for (int64_t r = 0; r < G.r; ++r) {
+            const int64_t nh = phh + G.ph - r * G.dh;  // = sigma_h * (p - i)
+            if (((nh % G.sh) + G.sh) % G.sh != 0) continue;
+            for (int64_t s = 0; s < G.s; ++s) {
+                const int64_t nw = phw + G.pw - s * G.dw;
+                if (((nw % G.sw) + G.sw) % G.sw != 0) continue;
+                const int k = p.taps.n + t;
+                p.taps.dh[k] = (int32_t)(nh / G.sh);
+                p.taps.dw[k] = (int32_t)(nw / G.sw);
+                p.taps.boff[k] = (int32_t)((r * G.s + s) * G.cg * G.kg);
+                ++t;
+            }
+        }
+        p.taps.n += t;
+        return t;
+    };
+    if (G.kg % 64 == 0 && G.sh * G.sw <= MAX_PHASES) {
+        // every stride phase in one launch; a phase without taps writes zeros
+        TNParams p = base;
+        p.taps.n = 0;
+        p.nphase = 0;
+        int64_t rows = 0, max_red = 0;
+        for (int64_t phh = 0; phh < G.sh; ++phh) {
+            for (int64_t phw = 0; phw < G.sw; ++phw) {
+                const int64_t mi = phh < G.h ? (G.h - phh + G.sh - 1) / G.sh : 0;
+                const int64_t mj = phw < G.w ? (G.w - phw + G.sw - 1) / G.sw : 0;
+                if (mi == 0 || mj == 0) continue;
+                const int start = p.taps.n;
+                const int cnt = add_phase_taps(p, phh, phw);
+                p.ph[p.nphase++] = phase_of(G.n * mi * mj, mi, mj, phh, phw, start, cnt);
+                rows += G.n * mi * mj;
+                if (cnt * G.kg > max_red) max_red = cnt * G.kg;
+            }
+        }
+        if (p.nphase == 0) return NNCONV_OK;
+        return hip_status(
+            launch_igemm_c64(G.dtype, pick_c64(rows, G.cg, max_red), p, pad, st));
+    }
+    // Otherwise sigma_h * sigma_w launches, one per output phase (h mod
+    // sigma_h, w mod sigma_w): within a phase every pixel sees the same set of
+    // contributing taps.  wt is [g][R][S][Cg][Kg].
     for (int64_t phh = 0; phh < G.sh; ++phh) {
         for (int64_t phw = 0; phw < G.sw; ++phw) {
             const int64_t mi = phh < G.h ? (G.h - phh + G.sh - 1) / G.sh : 0;
             const int64_t mj = phw < G.w ? (G.w - phw + G.sw - 1) / G.sw : 0;
             if (mi == 0 || mj == 0) continue;
-            TNParams p = tn_base();
-            p.a = dy;
-            p.a_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
-            p.b = wt;
-            p.b_bytes = (uint32_t)(G.k * G.r * G.s * G.cg * 2);
-            p.out = dx;
-            p.o_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+            TNParams p = base;
+            p.taps.n = 0;
+            const int t = add_phase_taps(p, phh, phw);
             p.mi = (int32_t)mi;
             p.mj = (int32_t)mj;
             p.M = (int32_t)(G.n * mi * mj);
             p.div_mj = make_fastdiv((uint32_t)mj);
             p.div_mi = make_fastdiv((uint32_t)mi);
-            p.a_h = (int32_t)G.p; p.a_w = (int32_t)G.q; p.a_c = (int32_t)G.k;
-            p.a_cg_ofs = (int32_t)G.kg;
-            p.ai_mul = 1; p.ai_add = 0; p.aj_mul = 1; p.aj_add = 0;
-            p.cr = (int32_t)G.kg;
-            p.div_crv = make_fastdiv((uint32_t)(G.kg / 8));
-            p.ncols = (int32_t)G.cg;
-            p.b_ld = (int32_t)G.kg;
-            p.b_g_ofs = (int32_t)(G.r * G.s * G.cg * G.kg);
-            p.o_h = (int32_t)G.h; p.o_w = (int32_t)G.w; p.o_c = (int32_t)G.c;
-            p.o_cg_ofs = (int32_t)G.cg;
-            p.oi_mul = (int32_t)G.sh; p.oi_add = (int32_t)phh;
-            p.oj_mul = (int32_t)G.sw; p.oj_add = (int32_t)phw;
-            p.alpha = alpha;
-            p.groups = (int32_t)G.g;
-            int t = 0;
-            for (int64_t r = 0; r < G.r; ++r) {
-                const int64_t nh = phh + G.ph - r * G.dh;  // = sigma_h * (p - i)
-                if (((nh % G.sh) + G.sh) % G.sh != 0) continue;
-                for (int64_t s = 0; s < G.s; ++s) {
-                    const int64_t nw = phw + G.pw - s * G.dw;
-                    if (((nw % G.sw) + G.sw) % G.sw != 0) continue;
-                    p.taps.dh[t] = (int32_t)(nh / G.sh);
-                    p.taps.dw[t] = (int32_t)(nw / G.sw);
-                    p.taps.boff[t] = (int32_t)((r * G.s + s) * G.cg * G.kg);
-                    ++t;
-                }
-            }
-            p.taps.n = t;
+            p.oi_add = (int32_t)phh;
+            p.oj_add = (int32_t)phw;
             p.k_iters = (int32_t)((int64_t(t) * G.kg + 63) / 64);
-            const bool pad = !(G.r == 1 && G.s == 1 && G.ph == 0 && G.pw == 0);
-            if (G.kg % 64 == 0)
-                TRY_HIP(launch_igemm_c64(G.dtype, pick_c64(p.M, G.cg, (int64_t)t * G.kg), p, pad, st));
-            else
+            if (G.kg % 64 == 0) {
+                p.nphase = 1;
+                p.ph[0] = phase_of(p.M, mi, mj, phh, phw, 0, t);
+                TRY_HIP(launch_igemm_c64(G.dtype, pick_c64(p.M, G.cg, (int64_t)t * G.kg), p, pad,
+                                         st));
+            } else {
                 TRY_HIP(launch_igemm_c8(G.dtype, pick_c8(G.cg), p, st));
+            }
         }
     }
     return NNCONV_OK;

@@ -103,13 +103,24 @@ void igemm_c64_kernel(const TNParams P) {
     const int wave = tid >> 6;
     const int wm = wave % WM, wn = wave / WM;
 
-    const uint32_t lid = xcd_remap(blockIdx.x, gridDim.x);
-    const int per_g = P.tiles_m * P.tiles_n;
-    const int g = (int)lid / per_g;
-    const int rem = (int)lid - g * per_g;
+    // phase of this workgroup: phases own consecutive ranges of hardware
+    // block ids, which the dispatcher deals round-robin to the XCDs, so every
+    // XCD gets a share of every phase; within a phase, consecutive tiles are
+    // then renumbered onto the same XCD
+    int phi = 0;
+    for (int i = 1; i < P.nphase; ++i)
+        if ((int)blockIdx.x >= P.ph[i].block_start) phi = i;
+    const TNPhase &F = P.ph[phi];
+    const int phase_blocks =
+        (phi + 1 < P.nphase ? P.ph[phi + 1].block_start : (int)gridDim.x) - F.block_start;
+    const int local = (int)xcd_remap(blockIdx.x - F.block_start, phase_blocks);
+    const int per_g = F.tiles_m * P.tiles_n;
+    const int g = local / per_g;
+    const int rem = local - g * per_g;
     const int tm = rem / P.tiles_n;
     const int tn = rem - tm * P.tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
+    const int tap0 = F.tap_start, ntaps = F.tap_count;
 
     // Staging role: load j of this wave fills rows (wave*LD + j)*RPI + lane/BKC,
     // physical chunk lane%BKC, i.e. logical chunk (lane%BKC) ^ swz(row).
@@ -125,11 +136,11 @@ void igemm_c64_kernel(const TNParams P) {
         const int lchunk = pch ^ swz<BKC>(r);
         const int m = m0 + r;
         a_mask[j] = 0;
-        if (m < P.M) {
-            const int q1 = (int)fdiv((uint32_t)m, P.div_mj);
-            const int jj = m - q1 * P.mj;
-            const int n = (int)fdiv((uint32_t)q1, P.div_mi);
-            const int ii = q1 - n * P.mi;
+        if (m < F.M) {
+            const int q1 = (int)fdiv((uint32_t)m, F.div_mj);
+            const int jj = m - q1 * F.mj;
+            const int n = (int)fdiv((uint32_t)q1, F.div_mi);
+            const int ii = q1 - n * F.mi;
             const int bh = ii * P.ai_mul + P.ai_add;
             const int bw = jj * P.aj_mul + P.aj_add;
             // byte offset of this row's base pixel and chunk (may wrap below 0
@@ -137,8 +148,8 @@ void igemm_c64_kernel(const TNParams P) {
             a_voff[j] = (uint32_t)(((n * P.a_h + bh) * P.a_w + bw) * P.a_c + g * P.a_cg_ofs) * 2u +
                         (uint32_t)lchunk * 16u;
             if constexpr (PAD) {
-                for (int t = 0; t < P.taps.n; ++t) {
-                    const int h = bh + P.taps.dh[t], w = bw + P.taps.dw[t];
+                for (int t = 0; t < ntaps; ++t) {
+                    const int h = bh + P.taps.dh[tap0 + t], w = bw + P.taps.dw[tap0 + t];
                     if ((unsigned)h < (unsigned)P.a_h && (unsigned)w < (unsigned)P.a_w)
                         a_mask[j] |= (uint64_t)1 << t;
                 }
@@ -161,7 +172,7 @@ void igemm_c64_kernel(const TNParams P) {
     int ld_t = 0, ld_c = 0;  // tap and channel base of the next slice to load
 
     auto issue = [&](int buf) {
-        const int t = ld_t;
+        const int t = tap0 + ld_t;
         // A: x / dy rows; the tap's pixel shift can be negative, so it is
         // added to the lane offsets; the channel base moves the descriptor
         const uint32_t ashift =
@@ -173,7 +184,7 @@ void igemm_c64_kernel(const TNParams P) {
         for (int j = 0; j < A_LD; ++j) {
             uint32_t off = a_voff[j] + ashift;
             if constexpr (PAD) {
-                if (!((a_mask[j] >> t) & 1)) off = OOB_OFFSET;
+                if (!((a_mask[j] >> ld_t) & 1)) off = OOB_OFFSET;
             } else {
                 if (a_voff[j] == OOB_OFFSET) off = OOB_OFFSET;
             }
@@ -184,7 +195,7 @@ void igemm_c64_kernel(const TNParams P) {
             dma16(sb + (uint32_t)(A_SLOTS + (wave * B_LD + j) * 64) * 16u, b_voff[j], db);
         // taps inner, channel slices outer: the taps of one channel slice
         // re-read overlapping pixels back to back, while they are still in L2
-        if (++ld_t == P.taps.n) {
+        if (++ld_t == ntaps) {
             ld_t = 0;
             ld_c += BK;
         }
@@ -198,7 +209,7 @@ void igemm_c64_kernel(const TNParams P) {
 
     const int l32 = lane & 31;
     const int khalf = lane >> 5;
-    const int k_iters = P.taps.n * (P.cr / BK);
+    const int k_iters = ntaps * (P.cr / BK);
 
     auto compute = [&](const u32x4 *st) {
 #pragma unroll
@@ -280,24 +291,30 @@ void igemm_c64_kernel(const TNParams P) {
         const int c = tid % CPR;
         const int m = m0 + r;
         const int ch = n0 + c * 8;
-        if (m >= P.M || ch >= P.ncols) continue;
-        const int q1 = (int)fdiv((uint32_t)m, P.div_mj);
-        const int jj = m - q1 * P.mj;
-        const int n = (int)fdiv((uint32_t)q1, P.div_mi);
-        const int ii = q1 - n * P.mi;
-        const int oh = ii * P.oi_mul + P.oi_add;
-        const int ow = jj * P.oj_mul + P.oj_add;
+        if (m >= F.M || ch >= P.ncols) continue;
+        const int q1 = (int)fdiv((uint32_t)m, F.div_mj);
+        const int jj = m - q1 * F.mj;
+        const int n = (int)fdiv((uint32_t)q1, F.div_mi);
+        const int ii = q1 - n * F.mi;
+        const int oh = ii * P.oi_mul + F.oi_add;
+        const int ow = jj * P.oj_mul + F.oj_add;
         const int64_t obase =
             ((int64_t)(n * P.o_h + oh) * P.o_w + ow) * P.o_c + (int64_t)g * P.o_cg_ofs;
-        *(u32x4 *)(out + obase + ch) = lds[r * CPR + (c ^ (r & CSW))];
+        // streaming store: the output is not read again by this pass, so it
+        // should not displace operand lines in L2
+        __builtin_nontemporal_store(lds[r * CPR + (c ^ (r & CSW))], (u32x4 *)(out + obase + ch));
     }
 }
 
 template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES>
 static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
-    p.tiles_m = (p.M + BM - 1) / BM;
     p.tiles_n = (p.ncols + BN - 1) / BN;
-    const int64_t nb = (int64_t)p.tiles_m * p.tiles_n * p.groups;
+    int64_t nb = 0;
+    for (int i = 0; i < p.nphase; ++i) {
+        p.ph[i].tiles_m = (p.ph[i].M + BM - 1) / BM;
+        p.ph[i].block_start = (int32_t)nb;
+        nb += (int64_t)p.ph[i].tiles_m * p.tiles_n * p.groups;
+    }
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (pad)

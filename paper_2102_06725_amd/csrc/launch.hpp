@@ -32,6 +32,20 @@ struct TapTable {
 // starts at element g*b_g_ofs + col*b_ld.  The result goes to pixel
 // (i*oi_mul + oi_add, j*oj_mul + oj_add) of an o_h x o_w image with o_c
 // channels, channel g*o_cg_ofs + col.
+// One output phase of a 64-channel-slice launch: rows m < M decode to
+// (image n, i < mi, j < mj); the output pixel is (i*oi_mul + oi_add,
+// j*oj_mul + oj_add); the phase uses taps [tap_start, tap_start + tap_count)
+// of the tap table.  The forward pass has one phase; backward-data has one per
+// stride phase, all in a single launch.
+struct TNPhase {
+    int32_t M, mi, mj;
+    FastDiv div_mj, div_mi;
+    int32_t oi_add, oj_add;
+    int32_t tap_start, tap_count;
+    int32_t tiles_m, block_start;  // filled by the launcher
+};
+constexpr int MAX_PHASES = 4;
+
 struct TNParams {
     const void *a;
     uint32_t a_bytes;
@@ -55,6 +69,8 @@ struct TNParams {
     int32_t groups;
     int32_t tiles_m, tiles_n;  // per group; filled by the launcher
     TapTable taps;
+    int32_t nphase;            // igemm_c64 only: phases in ph[]
+    TNPhase ph[MAX_PHASES];
 };
 
 // Any cr (a multiple of 8): the reduction is cut into slices of 32 elements

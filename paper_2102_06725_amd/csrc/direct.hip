@@ -181,14 +181,65 @@ __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__rest
     }
 }
 
+// Same transpose with 16-byte accesses on both sides (cols, dst_ld and rows
+// multiples of 8, 16-byte aligned buffers): a 64x64 tile is read as 8-element
+// row chunks, and each output chunk gathers 8 consecutive rows of one column
+// from LDS.
+__global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__restrict__ src,
+                                                              uint16_t *__restrict__ dst,
+                                                              int64_t rows, int64_t cols,
+                                                              int64_t dst_ld, int64_t tiles_c,
+                                                              int64_t tiles_r) {
+    constexpr int LD = 72;  // halves per LDS row (144 bytes: 16-byte aligned, skewed)
+    __shared__ uint16_t tile[64 * LD];
+    const int64_t t = blockIdx.x;
+    const int64_t b = t / (tiles_c * tiles_r);
+    const int64_t rem = t - b * tiles_c * tiles_r;
+    const int64_t tr = rem / tiles_c, tc = rem - (rem / tiles_c) * tiles_c;
+    const int64_t r0 = tr * 64, c0 = tc * 64;
+    const uint16_t *s = src + b * rows * cols;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int id = threadIdx.x + 256 * i;
+        const int row = id >> 3, cc = (id & 7) * 8;
+        const int64_t rr = r0 + row, col = c0 + cc;
+        u32x4 v = u32x4{};
+        if (rr < rows && col < cols) v = *(const u32x4 *)(s + rr * cols + col);
+        *(u32x4 *)(&tile[row * LD + cc]) = v;
+    }
+    __syncthreads();
+    uint16_t *d = dst + b * cols * dst_ld;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int id = threadIdx.x + 256 * i;
+        const int oc = id >> 3, rc = (id & 7) * 8;
+        const int64_t col = c0 + oc, rr = r0 + rc;
+        if (col < cols && rr < dst_ld) {
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                w[e] = (uint32_t)tile[(rc + 2 * e) * LD + oc] |
+                       ((uint32_t)tile[(rc + 2 * e + 1) * LD + oc] << 16);
+            *(u32x4 *)(d + col * dst_ld + rr) = u32x4{w[0], w[1], w[2], w[3]};
+        }
+    }
+}
+
 hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
                               int64_t cols, int64_t dst_ld, hipStream_t st) {
     const int64_t tiles_c = (cols + 63) / 64, tiles_r = (dst_ld + 63) / 64;
     const int64_t nb = batch * tiles_c * tiles_r;
     if (nb <= 0) return hipSuccess;
-    hipLaunchKernelGGL(transpose16_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
-                       (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
-                       tiles_r);
+    const bool vec = cols % 8 == 0 && dst_ld % 8 == 0 && rows % 8 == 0 &&
+                     (uintptr_t)src % 16 == 0 && (uintptr_t)dst % 16 == 0;
+    if (vec)
+        hipLaunchKernelGGL(transpose16_vec_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
+                           (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
+                           tiles_r);
+    else
+        hipLaunchKernelGGL(transpose16_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
+                           (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
+                           tiles_r);
     return hipGetLastError();
 }
 

@@ -185,6 +185,27 @@ def test_wgrad_unaligned_dw(dw_dtype):
     assert orc.rel_err(to_nchw(case, "dw", b["dw"]), ref) <= (1e-5 if dw_dtype == "f32" else TOL[I.F16])
 
 
+def test_transforms_vector_path_bit_exact():
+    """Sizes that take the 16-byte transpose path (multiples of 8), with
+    ragged 64x64 tiles and channel padding."""
+    tt = torch()
+    rng = np.random.default_rng(4)
+    s = stream()
+    n, c, h, w, cp = 2, 72, 5, 16, 80
+    src = rng.integers(0, 65535, size=(n, c, h, w), dtype=np.uint16)
+    out = Guarded(n * h * w * cp)
+    nc.check(nc.nnconv_nchw_to_nhwc(to_dev(src).data_ptr(), out.ptr(), n, c, h, w, cp, s))
+    tt.cuda.synchronize()
+    ref = np.zeros((n, h, w, cp), np.uint16)
+    ref[..., :c] = src.transpose(0, 2, 3, 1)
+    assert np.array_equal(out.host().reshape(n, h, w, cp), ref)
+    nhwc = np.ascontiguousarray(src.transpose(0, 2, 3, 1))
+    back = Guarded(n * c * h * w)
+    nc.check(nc.nnconv_nhwc_to_nchw(to_dev(nhwc).data_ptr(), back.ptr(), n, c, h, w, s))
+    tt.cuda.synchronize()
+    assert np.array_equal(back.host().reshape(src.shape), src)
+
+
 def test_transforms_bit_exact():
     tt = torch()
     rng = np.random.default_rng(3)

@@ -161,7 +161,7 @@ def write_per_layer(path, layers, ev_steps, steps):
 
 # Sources that determine the forward launches (dispatch plans and kernels);
 # stored HBM-traffic counters are reported only while these are unchanged.
-FWD_SOURCES = ("api.hip", "common.hpp", "igemm_c8.hip", "igemm_c64.hip", "launch.hpp")
+FWD_SOURCES = ("api.hip", "common.hpp", "igemm_c8.hip", "igemm_c64.hip", "launch.hpp", "stem.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "igemm_fwd_traffic_resnet50_b256.txt")
 COPY_ROW_BYTES = 128    # calibration copy: rows of 64 fp16 channels
 
@@ -196,11 +196,11 @@ def stored_traffic():
 def is_forward_launch(names, i):
     """In this script's launch order (flag clear, then per layer: optional
     stem channel padding, forward, backward-data kernels, backward-weight
-    kernel and its reduction) a forward launch is an implicit-GEMM dispatch
-    that follows a non-library dispatch, a split reduction or a padding
-    copy."""
+    kernel and its reduction) a forward launch is an implicit-GEMM or stem
+    dispatch that follows a non-library dispatch, a split reduction or a
+    padding copy."""
     n = names[i]
-    if "nnconv::" not in n or "igemm" not in n:
+    if "nnconv::" not in n or not ("igemm" in n or "stem_fwd" in n):
         return False
     if i == 0:
         return True
@@ -433,7 +433,7 @@ def main():
         ach = fwd_avg_flops / (fwd_avg_ms * 1e-3) / 1e12
         traffic = stored_traffic() if args.workload == "sweep" and not args.layers and \
             not args.batch and args.dtype == "f16" else None
-        roofline = {"kernel": "forward implicit GEMM (igemm_c64_kernel; igemm_c8_kernel for "
+        roofline = {"kernel": "forward implicit GEMM (igemm_c64_kernel; stem_fwd_kernel for "
                               "the stem), one launch per nnconv_fwd call",
                     "bound": "mfma", "achieved": ach, "peak": PEAK_F16_TFLOPS,
                     "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS, "traffic": traffic,

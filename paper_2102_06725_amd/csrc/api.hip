@@ -90,11 +90,13 @@ struct WgPlan {
 // ResNet-50 layers at batch 256: 256x256 tiles and about 256 workgroups
 // (long pixel ranges, few partial tiles to write and reduce) when both GEMM
 // sides are at least 256 wide; 64-row tiles and more pixel splits (1024
-// workgroups) when Kg <= 64; otherwise 128x128 tiles and 512 workgroups.
+// workgroups) when Kg <= 64; otherwise 128x128 tiles and 512 workgroups,
+// single-stage for very wide filters (R*S*Cg >= 4096), where more resident
+// workgroups per CU pay off.
 WGConfig pick_wg(int64_t kg, int64_t rscg) {
     if (kg <= 64) return WG_64x128;
     if (kg >= 256 && rscg >= 256 && rscg < 4096) return WG_256x256;
-    return WG_128x128;
+    return rscg >= 4096 ? WG_128x128S : WG_128x128;
 }
 
 int64_t wg_target_blocks(WGConfig cfg) {
@@ -113,8 +115,8 @@ WgPlan plan_wgrad_fast(const Geom &G) {
     }
     const int64_t rscg = G.r * G.s * G.cg;
     pl.cfg = pick_wg(G.kg, rscg);
-    static const int64_t tile_m[] = {128, 64, 256};
-    static const int64_t tile_n[] = {128, 128, 256};
+    static const int64_t tile_m[] = {128, 64, 256, 128};
+    static const int64_t tile_n[] = {128, 128, 256, 128};
     const int64_t bmk = tile_m[pl.cfg], bnj = tile_n[pl.cfg];
     const int64_t tiles = G.g * ((G.kg + bmk - 1) / bmk) * ((rscg + bnj - 1) / bnj);
     const int64_t npq = G.n * G.p * G.q;

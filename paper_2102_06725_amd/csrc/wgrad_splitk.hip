@@ -77,7 +77,10 @@ __device__ __forceinline__ uint32_t tile_off(int p, int co) {
 }  // namespace wgs
 
 template <class T, int BM, int BN, int WM, int WN, int BKP, int STAGES>
-__global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 1024) ? 1 : 2) void wgrad_splitk_kernel(const WGParams P) {
+__global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 1024) ? 1
+                                           : (STAGES * BKP * (BM + BN) * 2 > 40 * 1024) ? 2
+                                                                                       : 4)
+void wgrad_splitk_kernel(const WGParams P) {
     using namespace wgs;
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -216,7 +219,32 @@ __global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 
         return r;
     };
 
-    if (k_iters > 0) {
+    auto compute = [&](int buf) {
+        const char *st = (const char *)&lds[0] + buf * STAGE_BYTES;
+#pragma unroll
+        for (int ks = 0; ks < BKP / 16; ++ks) {
+            u32x4 fa[FM], fb[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) fa[i] = frag(st, 1, ks, wm * WTM + i * 32);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) fb[j] = frag(st + A_BYTES, 0, ks, wn * WTN + j * 32);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<T>(fa[i], fb[j], acc[i][j]);
+        }
+    };
+    if constexpr (STAGES == 1) {
+        // one stage: several resident workgroups per CU cover each other's
+        // load latency
+        for (int kt = 0; kt < k_iters; ++kt) {
+            if (kt > 0) barrier_lds();  // previous slice fully read
+            issue(kt, 0);
+            wait_vmcnt<0>();
+            barrier_lds();
+            compute(0);
+        }
+    } else if (k_iters > 0) {
         const int pro = k_iters < STAGES - 1 ? k_iters : STAGES - 1;
         for (int s = 0; s < pro; ++s) issue(s, s);
         for (int kt = 0; kt < k_iters; ++kt) {
@@ -226,19 +254,7 @@ __global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 
                 wait_vmcnt<0>();
             barrier_lds();
             if (kt + STAGES - 1 < k_iters) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-            const char *st = (const char *)&lds[0] + (kt % STAGES) * STAGE_BYTES;
-#pragma unroll
-            for (int ks = 0; ks < BKP / 16; ++ks) {
-                u32x4 fa[FM], fb[FN];
-#pragma unroll
-                for (int i = 0; i < FM; ++i) fa[i] = frag(st, 1, ks, wm * WTM + i * 32);
-#pragma unroll
-                for (int j = 0; j < FN; ++j) fb[j] = frag(st + A_BYTES, 0, ks, wn * WTN + j * 32);
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<T>(fa[i], fb[j], acc[i][j]);
-            }
+            compute(kt % STAGES);
         }
     }
 
@@ -274,14 +290,19 @@ static hipError_t launch_wgs(WGParams &p, hipStream_t st) {
 }
 
 // Configurations (LDS per workgroup):
-//    64x128: 4 waves of 32x64, 32-pixel slices, 3 stages (36 KB)
+//    64x128: 4 waves of 32x64, 64-pixel slices, single stage (24 KB)
 //   128x128: 4 waves of 64x64, 32-pixel slices, 3 stages (48 KB)
-//   256x256: 8 waves of 128x64, 32-pixel slices, 3 stages (96 KB)
+//   128x128 single stage: 64-pixel slices (32 KB; four workgroups per CU)
+//   256x256: 8 waves of 128x64, 32-pixel slices, 2 stages (64 KB)
 template <class T>
 static hipError_t launch_wgs_t(WGConfig cfg, WGParams &p, hipStream_t st) {
-    if (cfg == WG_64x128) return launch_wgs<T, 64, 128, 2, 2, 32, 3>(p, st);
-    if (cfg == WG_256x256) return launch_wgs<T, 256, 256, 2, 4, 32, 3>(p, st);
-    return launch_wgs<T, 128, 128, 2, 2, 32, 3>(p, st);
+    switch (cfg) {
+        case WG_64x128: return launch_wgs<T, 64, 128, 2, 2, 64, 1>(p, st);
+        case WG_256x256: return launch_wgs<T, 256, 256, 2, 4, 32, 2>(p, st);
+        case WG_128x128S: return launch_wgs<T, 128, 128, 2, 2, 64, 1>(p, st);
+        case WG_128x128:
+        default: return launch_wgs<T, 128, 128, 2, 2, 32, 3>(p, st);
+    }
 }
 
 hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st) {

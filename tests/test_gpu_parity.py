@@ -79,6 +79,7 @@ SMALL = [
     ("1x1 C192 K96", Case(L("s7", 2, 192, 7, 9, 96, 1, 1))),
     ("3x3 stride 3 C64 K64 (nine phases)", Case(L("s9", 2, 64, 13, 14, 64, 3, 3, 3, 1))),
     ("1x1 stride 2 C128 K256 (zero phases)", Case(L("s10", 3, 128, 9, 10, 256, 1, 1, 2, 0))),
+    ("3x3 C512 K128 (wide filter)", Case(L("s11", 2, 512, 5, 6, 128, 3, 3, 1, 1))),
     ("3x3 C256 K512 bf16", Case(L("s8", 2, 256, 6, 5, 512, 3, 3, 1, 1), dtype=I.BF16)),
     ("P = Q = 1", Case(L("s", 2, 16, 3, 3, 16, 3, 3, 1, 0))),
     ("H = W = 1, 1x1", Case(L("t", 5, 32, 1, 1, 24, 1, 1))),

@@ -319,6 +319,47 @@ def cpu_baseline(args, wl):
     }
 
 
+UPDATE_BYTES_PER_PARAM = 22  # read master, momentum, grad (fp32); write master, momentum, w16
+
+
+def measure_update(args, layers, torch, nc, dev, sptr, stream, reps=20):
+    """Times the fused fp32 master-weight update (momentum SGD, loss-scale
+    division, 16-bit copy) over every weight of the workload's layers held in
+    one flat buffer -- outside the convolution metric, reported beside it."""
+    count = sum(L.k * (L.c_alg // L.groups) * L.r * L.s for L in layers)
+    count = (count + 3) // 4 * 4
+    g = torch.Generator(device="cpu").manual_seed(5)
+    master = (torch.randn(count, generator=g) * 0.05).to(dev)
+    mom = torch.zeros(count, dtype=torch.float32, device=dev)
+    grad = (torch.randn(count, generator=g) * 20.0).to(dev)
+    w16 = torch.empty(count, dtype=torch.int16, device=dev)
+    state = torch.zeros(6, dtype=torch.int32, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    nc.check(nc.nnconv_loss_scaler_init(state.data_ptr(), 1024.0, 2.0, 2000, sptr), "scaler")
+    w16_dtype = nc.NNCONV_F16 if args.dtype == "f16" else nc.NNCONV_BF16
+
+    def call():
+        nc.check(nc.nnconv_sgd_update(count, master.data_ptr(), mom.data_ptr(), w16.data_ptr(),
+                                      w16_dtype, grad.data_ptr(), state.data_ptr(),
+                                      flag.data_ptr(), 0.1, 0.9, 1e-4, sptr), "sgd_update")
+
+    for _ in range(3):
+        call()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    gbps = count * UPDATE_BYTES_PER_PARAM / (us * 1e-6) / 1e9
+    return {"kernel": "sgd_update_kernel (one launch over all %d conv weights)" % count,
+            "params": count, "us_per_launch": us, "bound": "hbm",
+            "achieved": gbps, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": gbps / PEAK_HBM_GBS}
+
+
 def main():
     args = parse()
     if args.summarize_profile:
@@ -440,6 +481,8 @@ def main():
                     "avg_launch_us": fwd_avg_ms * 1e3,
                     "avg_flops_per_launch": fwd_avg_flops}
 
+    update = measure_update(args, layers, torch, nc, dev, sptr, stream) if use_ev else None
+
     if args.per_layer and use_ev:
         write_per_layer(args.per_layer, layers, ev_steps, args.steps)
 
@@ -470,6 +513,7 @@ def main():
         "per_pass": per_pass,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "update": update,
     }
     print(json.dumps(out), flush=True)
 

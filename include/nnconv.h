@@ -152,6 +152,82 @@ nnconv_status nnconv_weight_kcrs_to_krsc(const void *src, void *dst, int32_t k, 
 nnconv_status nnconv_weight_krsc_to_kcrs(const void *src, void *dst, int32_t k, int32_t cg,
                                          int32_t r, int32_t s, void *hip_stream);
 
+/* Training-step pieces after the backward passes (Sec. 3.3, Listing 6).
+ *
+ * A step with dynamic loss scaling, all on one stream and with no host
+ * synchronisation:
+ *   1. the caller seeds dy of the loss with the current scale S (it can read
+ *      S from the device state below, e.g. as a 0-d tensor view);
+ *   2. nnconv_wgrad for every layer with inv_loss_scale = 1, dw_dtype F32
+ *      and one shared overflow flag (zeroed once, at set-up);
+ *   3. nnconv_sgd_update for every parameter array, passing the state and
+ *      the flag: it divides the gradient by S and does nothing at all when
+ *      the flag is set;
+ *   4. nnconv_loss_scaler_update once: it advances the scaler by the flag
+ *      and clears the flag for the next step.
+ * The order 3-before-4 matters: the update uses the scale the gradients
+ * were computed with, and the scale only grows afterwards, as in the
+ * listing. */
+
+/* Device-resident dynamic loss-scaler state (24 bytes, caller-owned device
+ * memory, 4-byte aligned).  Readable by the caller at any time; written
+ * only by the two calls below. */
+typedef struct {
+    float scale;      /* current loss scale S */
+    float factor;     /* growth / shrink factor (2 in the paper) */
+    int32_t interval; /* clean steps between growths (2000 in the paper) */
+    int32_t counter;  /* clean steps since the last growth or overflow */
+    int32_t skipped;  /* steps skipped because of an inf or NaN gradient */
+    int32_t reserved; /* zero */
+} nnconv_loss_scaler;
+
+/* Queues the initialisation of *state: scale = initial_scale, factor,
+ * interval, counter = skipped = 0.
+ * INVALID_ARG: null state, initial_scale or factor not finite and > 0,
+ * interval < 0.  MISALIGNED: state not 4-byte aligned. */
+nnconv_status nnconv_loss_scaler_init(nnconv_loss_scaler *state, float initial_scale,
+                                      float factor, int32_t interval, void *hip_stream);
+
+/* One step of the dynamic scaler of Listing 6, driven by *overflow_flag (a
+ * device int32, nonzero = this step's gradients held an inf or a NaN):
+ *   flag set:   scale /= factor; counter = 0; skipped += 1
+ *   flag clear: if counter > interval { scale *= factor; counter = 0 }
+ *               counter += 1
+ * and then *overflow_flag = 0.  The test runs before the increment, so with
+ * interval 2000 the first growth comes on the 2002nd consecutive clean step
+ * and later ones every 2001 clean steps.  One thread; queue it after every
+ * nnconv_sgd_update of the step.
+ * INVALID_ARG: null pointer.  MISALIGNED: either pointer not 4-byte
+ * aligned. */
+nnconv_status nnconv_loss_scaler_update(nnconv_loss_scaler *state, int32_t *overflow_flag,
+                                        void *hip_stream);
+
+/* fp32 master-weight update (Sec. 3.3: 16-bit working weights, fp32 master
+ * copy updated in fp32).  The paper names no solver; this is momentum SGD
+ * with L2 weight decay, element-wise over count entries:
+ *   g = grad / S + weight_decay * master      (S = state->scale, 1 if NULL)
+ *   momentum = momentum_coef * momentum + g
+ *   master  -= lr * momentum
+ *   w16      = round-to-nearest-even(master)  (when w16 is not NULL)
+ * computed in fp32 (1/S taken once, so a power-of-two S is exact).
+ * master, momentum, grad: device fp32 arrays of count elements, in any
+ * common element order (the nnconv_wgrad dw order of the layer's layout
+ * matches the weights).  w16: NULL or device array of count elements of
+ * w16_dtype (F16 or BF16), e.g. the layer's weights for the next forward.
+ * overflow_flag: NULL or the step's device flag; when it is nonzero the
+ * call changes nothing (the step is skipped).  The flag is only read.
+ * In-place; master, momentum, grad and w16 must not overlap.  count = 0 is
+ * a no-op.  16-byte aligned arrays and count % 4 == 0 take a vectorised
+ * path.
+ * INVALID_ARG: count < 0, null master/momentum/grad, w16_dtype not F16 or
+ * BF16 when w16 is given.  MISALIGNED: fp32 arrays or state/flag not 4-byte
+ * aligned, w16 not 2-byte aligned. */
+nnconv_status nnconv_sgd_update(int64_t count, float *master, float *momentum, void *w16,
+                                int32_t w16_dtype, const float *grad,
+                                const nnconv_loss_scaler *state, const int32_t *overflow_flag,
+                                float lr, float momentum_coef, float weight_decay,
+                                void *hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

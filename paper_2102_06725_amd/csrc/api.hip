@@ -708,3 +708,48 @@ NNCONV_API nnconv_status nnconv_weight_krsc_to_kcrs(const void *src, void *dst, 
     return hip_status(launch_transpose16(src, dst, k, (int64_t)r * s, cg, (int64_t)r * s,
                                          (hipStream_t)hip_stream));
 }
+
+// ---------------------------------------------------------------------------
+// training-step pieces: dynamic loss scaler and fp32 master-weight update
+// ---------------------------------------------------------------------------
+
+NNCONV_API nnconv_status nnconv_loss_scaler_init(nnconv_loss_scaler *state, float initial_scale,
+                                                 float factor, int32_t interval,
+                                                 void *hip_stream) {
+    if (!state || interval < 0) return NNCONV_ERR_INVALID_ARG;
+    if (!(initial_scale > 0.0f) || !(factor > 0.0f) || !__builtin_isfinite(initial_scale) ||
+        !__builtin_isfinite(factor))
+        return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(state, 4)) return NNCONV_ERR_MISALIGNED;
+    clear_stale_error();
+    return hip_status(
+        launch_loss_scaler_init(state, initial_scale, factor, interval, (hipStream_t)hip_stream));
+}
+
+NNCONV_API nnconv_status nnconv_loss_scaler_update(nnconv_loss_scaler *state,
+                                                   int32_t *overflow_flag, void *hip_stream) {
+    if (!state || !overflow_flag) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(state, 4) || !aligned(overflow_flag, 4)) return NNCONV_ERR_MISALIGNED;
+    clear_stale_error();
+    return hip_status(launch_loss_scaler_update(state, overflow_flag, (hipStream_t)hip_stream));
+}
+
+NNCONV_API nnconv_status nnconv_sgd_update(int64_t count, float *master, float *momentum,
+                                           void *w16, int32_t w16_dtype, const float *grad,
+                                           const nnconv_loss_scaler *state,
+                                           const int32_t *overflow_flag, float lr,
+                                           float momentum_coef, float weight_decay,
+                                           void *hip_stream) {
+    if (count < 0 || count > MAX_ELEMS || !master || !momentum || !grad)
+        return NNCONV_ERR_INVALID_ARG;
+    if (w16 && w16_dtype != NNCONV_F16 && w16_dtype != NNCONV_BF16) return NNCONV_ERR_INVALID_ARG;
+    if (!aligned(master, 4) || !aligned(momentum, 4) || !aligned(grad, 4) ||
+        (w16 && !aligned(w16, 2)) || (state && !aligned(state, 4)) ||
+        (overflow_flag && !aligned(overflow_flag, 4)))
+        return NNCONV_ERR_MISALIGNED;
+    if (count == 0) return NNCONV_OK;
+    clear_stale_error();
+    return hip_status(launch_sgd_update(count, master, momentum, w16, w16_dtype, grad, state,
+                                        overflow_flag, lr, momentum_coef, weight_decay,
+                                        (hipStream_t)hip_stream));
+}

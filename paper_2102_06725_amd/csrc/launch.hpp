@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "common.hpp"
+#include "nnconv.h"
 
 namespace nnconv {
 
@@ -167,5 +168,13 @@ hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t
 // dst[row][ch] = ch < c ? src[row][ch] : 0   for ch < c_pad
 hipError_t launch_pad_channels16(const void *src, void *dst, int64_t rows, int32_t c,
                                  int32_t c_pad, hipStream_t st);
+
+// Training-step pieces (update.hip).  The state type is the C ABI's.
+hipError_t launch_loss_scaler_init(nnconv_loss_scaler *s, float scale, float factor,
+                                   int32_t interval, hipStream_t st);
+hipError_t launch_loss_scaler_update(nnconv_loss_scaler *s, int32_t *flag, hipStream_t st);
+hipError_t launch_sgd_update(int64_t count, float *master, float *mom, void *w16, int w16_dtype,
+                             const float *grad, const nnconv_loss_scaler *state,
+                             const int32_t *flag, float lr, float mu, float wd, hipStream_t st);
 
 }  // namespace nnconv

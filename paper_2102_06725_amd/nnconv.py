@@ -36,13 +36,21 @@ NNCONV_WGRAD = 2
 EXPORTS = ("nnconv_version", "nnconv_last_hip_error", "nnconv_status_string", "nnconv_output_dims",
            "nnconv_workspace_size", "nnconv_fwd", "nnconv_dgrad", "nnconv_wgrad",
            "nnconv_nchw_to_nhwc", "nnconv_nhwc_to_nchw", "nnconv_pad_channels",
-           "nnconv_weight_kcrs_to_krsc", "nnconv_weight_krsc_to_kcrs")
+           "nnconv_weight_kcrs_to_krsc", "nnconv_weight_krsc_to_kcrs",
+           "nnconv_loss_scaler_init", "nnconv_loss_scaler_update", "nnconv_sgd_update")
 
 
 class nnconv_desc(ctypes.Structure):
     _fields_ = [(f, ctypes.c_int32) for f in
                 ("n", "c", "h", "w", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
                  "dil_h", "dil_w", "groups", "layout", "dtype")]
+
+
+class nnconv_loss_scaler(ctypes.Structure):
+    """Layout of the device-resident scaler state (24 bytes)."""
+    _fields_ = [("scale", ctypes.c_float), ("factor", ctypes.c_float),
+                ("interval", ctypes.c_int32), ("counter", ctypes.c_int32),
+                ("skipped", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class NNConvError(RuntimeError):
@@ -96,6 +104,10 @@ def load(path: str | None = None):
     lib.nnconv_pad_channels.argtypes = [_VP, _VP, _I64, _I32, _I32, _VP]
     lib.nnconv_weight_kcrs_to_krsc.argtypes = [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _VP]
     lib.nnconv_weight_krsc_to_kcrs.argtypes = [_VP, _VP, _I32, _I32, _I32, _I32, _VP]
+    lib.nnconv_loss_scaler_init.argtypes = [_VP, ctypes.c_float, ctypes.c_float, _I32, _VP]
+    lib.nnconv_loss_scaler_update.argtypes = [_VP, _VP, _VP]
+    lib.nnconv_sgd_update.argtypes = [_I64, _VP, _VP, _VP, _I32, _VP, _VP, _VP, ctypes.c_float,
+                                      ctypes.c_float, ctypes.c_float, _VP]
     for f in EXPORTS[3:]:
         getattr(lib, f).restype = ctypes.c_int
     if path is None:
@@ -174,6 +186,22 @@ def nnconv_weight_kcrs_to_krsc(src, dst, k, cg, r, s, cg_pad, stream) -> int:
 
 def nnconv_weight_krsc_to_kcrs(src, dst, k, cg, r, s, stream) -> int:
     return load().nnconv_weight_krsc_to_kcrs(src, dst, k, cg, r, s, stream)
+
+
+def nnconv_loss_scaler_init(state, initial_scale, factor, interval, stream) -> int:
+    return load().nnconv_loss_scaler_init(state, float(initial_scale), float(factor),
+                                          int(interval), stream)
+
+
+def nnconv_loss_scaler_update(state, overflow_flag, stream) -> int:
+    return load().nnconv_loss_scaler_update(state, overflow_flag, stream)
+
+
+def nnconv_sgd_update(count, master, momentum, w16, w16_dtype, grad, state, overflow_flag, lr,
+                      momentum_coef, weight_decay, stream) -> int:
+    return load().nnconv_sgd_update(int(count), master, momentum, w16, int(w16_dtype), grad,
+                                    state, overflow_flag, float(lr), float(momentum_coef),
+                                    float(weight_decay), stream)
 
 
 def check(status: int, what: str = "") -> None:

@@ -133,3 +133,43 @@ def test_transform_validation(nnlib):
     assert nc.nnconv_weight_kcrs_to_krsc(FAKE, FAKE, 4, 3, 3, 3, 2, None) == nc.NNCONV_ERR_INVALID_ARG
     assert nc.nnconv_weight_krsc_to_kcrs(FAKE, FAKE, 0, 3, 3, 3, None) == nc.NNCONV_ERR_INVALID_ARG
     assert nc.nnconv_nhwc_to_nchw(FAKE, None, 1, 3, 4, 4, None) == nc.NNCONV_ERR_INVALID_ARG
+
+
+def test_loss_scaler_state_layout():
+    assert ctypes.sizeof(nc.nnconv_loss_scaler) == 24
+    assert [f for f, _ in nc.nnconv_loss_scaler._fields_] == [
+        "scale", "factor", "interval", "counter", "skipped", "reserved"]
+
+
+def test_loss_scaler_validation(nnlib):
+    inv, mis = nc.NNCONV_ERR_INVALID_ARG, nc.NNCONV_ERR_MISALIGNED
+    assert nc.nnconv_loss_scaler_init(None, 1024.0, 2.0, 2000, None) == inv
+    assert nc.nnconv_loss_scaler_init(FAKE, 0.0, 2.0, 2000, None) == inv
+    assert nc.nnconv_loss_scaler_init(FAKE, -1.0, 2.0, 2000, None) == inv
+    assert nc.nnconv_loss_scaler_init(FAKE, float("inf"), 2.0, 2000, None) == inv
+    assert nc.nnconv_loss_scaler_init(FAKE, float("nan"), 2.0, 2000, None) == inv
+    assert nc.nnconv_loss_scaler_init(FAKE, 1024.0, 0.0, 2000, None) == inv
+    assert nc.nnconv_loss_scaler_init(FAKE, 1024.0, 2.0, -1, None) == inv
+    assert nc.nnconv_loss_scaler_init(FAKE + 2, 1024.0, 2.0, 2000, None) == mis
+    assert nc.nnconv_loss_scaler_update(None, FAKE, None) == inv
+    assert nc.nnconv_loss_scaler_update(FAKE, None, None) == inv
+    assert nc.nnconv_loss_scaler_update(FAKE, FAKE + 1, None) == mis
+
+
+def test_sgd_update_validation(nnlib):
+    inv, mis = nc.NNCONV_ERR_INVALID_ARG, nc.NNCONV_ERR_MISALIGNED
+
+    def call(count=16, master=FAKE, mom=FAKE, w16=FAKE, w16_dtype=nc.NNCONV_F16, grad=FAKE,
+             state=FAKE, flag=FAKE):
+        return nc.nnconv_sgd_update(count, master, mom, w16, w16_dtype, grad, state, flag,
+                                    0.1, 0.9, 1e-4, None)
+
+    assert call(count=-1) == inv
+    assert call(master=None) == inv and call(mom=None) == inv and call(grad=None) == inv
+    assert call(w16_dtype=nc.NNCONV_F32) == inv
+    assert call(master=FAKE + 2) == mis and call(mom=FAKE + 2) == mis
+    assert call(grad=FAKE + 1) == mis and call(w16=FAKE + 1) == mis
+    assert call(state=FAKE + 2) == mis and call(flag=FAKE + 2) == mis
+    # count 0 is a no-op that touches nothing, w16 NULL ignores w16_dtype
+    assert call(count=0) == nc.NNCONV_OK
+    assert call(count=0, w16=None, w16_dtype=7, state=None, flag=None) == nc.NNCONV_OK

@@ -253,13 +253,18 @@ C8Config pick_c8(int64_t ncols) { return ncols <= 64 ? C8_256x64 : C8_128x128; }
 //     problems);
 //   - otherwise the single-stage 128-row tiles, 3-5 per CU, hide each
 //     other's load latency best; very long reductions prefer the pipelined
-//     128x128 tile.
+//     128x128 tile;
+//   - a 256x256 tile run by 16 waves (four per SIMD) beats both for 256
+//     output columns with long reductions on 100-256 row tiles.
 constexpr int64_t MIN_BIG_TILES = 160;
 constexpr int64_t BIG_RED = 2048;
 constexpr int64_t LONG_RED = 4096;
 
 C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
     if (ncols <= 64) return C64S_128x64;
+    // 256 output columns, long reductions, about 200 tiles of 256 rows (the
+    // 14x14 layers at batch 256): the 16-wave 256x256 tile
+    if (ncols == 256 && red >= 1024 && m > 98 * 256 && m <= 256 * 256) return C64W_256x256;
     const int64_t big_tiles = ((m + 255) / 256) * ((ncols + 255) / 256);
     if (ncols >= 256 && red >= BIG_RED && big_tiles >= MIN_BIG_TILES) return C64_256x256;
     return red >= LONG_RED ? C64_128x128 : C64S_128x128;
@@ -335,13 +340,22 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     p.oi_mul = 1; p.oi_add = 0; p.oj_mul = 1; p.oj_add = 0;
     p.alpha = alpha;
     p.groups = (int32_t)G.g;
+    // Tap order of the 64-channel-slice kernel: the centre tap first.  Its
+    // slice reads the tile's own pixels (first touch, from HBM); the other
+    // taps then read pixels already in L2 (the tile's own or its
+    // neighbours', whose centre slices run at the same time on the same
+    // XCD), so fewer slices wait on HBM latency.  Any order gives the same
+    // sum up to fp32 rounding.
+    const int ntap = (int)(G.r * G.s);
+    const int t0 = G.cg % 64 == 0 ? (int)((G.r / 2) * G.s + G.s / 2) : 0;
     int t = 0;
-    for (int r = 0; r < G.r; ++r)
-        for (int s = 0; s < G.s; ++s, ++t) {
-            p.taps.dh[t] = (int32_t)(r * G.dh);
-            p.taps.dw[t] = (int32_t)(s * G.dw);
-            p.taps.boff[t] = (int32_t)(t * G.cg);
-        }
+    for (int u = 0; u < ntap; ++u, ++t) {
+        const int lin = (u + t0) % ntap;
+        const int r = lin / (int)G.s, s = lin % (int)G.s;
+        p.taps.dh[t] = (int32_t)(r * G.dh);
+        p.taps.dw[t] = (int32_t)(s * G.dw);
+        p.taps.boff[t] = (int32_t)(lin * G.cg);
+    }
     p.taps.n = t;
     p.k_iters = (int32_t)((int64_t(t) * G.cg + 63) / 64);
     if (G.cg % 64 == 0) {

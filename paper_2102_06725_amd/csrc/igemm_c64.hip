@@ -328,6 +328,8 @@ static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
 
 // Configurations (LDS per workgroup in parentheses):
 //   256x256: 8 waves of 128x64, 64-element slices, 2 stages (128 KB)
+//   256x256 wide: 16 waves of 64x64, same LDS; four waves per SIMD hide
+//            the fragment-read latency better on some mid-size layers
 //   128x128: 4 waves of 64x64, 64-element slices, 2 stages (64 KB; two
 //            workgroups per CU)
 // Single-stage tiles, whose small LDS footprint lets 3-5 workgroups share a
@@ -337,6 +339,7 @@ template <class T>
 static hipError_t launch_c64_t(C64Config cfg, TNParams &p, bool pad, hipStream_t st) {
     switch (cfg) {
         case C64_256x256: return launch_c64_cfg<T, 256, 256, 2, 4, 8, 2>(p, pad, st);
+        case C64W_256x256: return launch_c64_cfg<T, 256, 256, 4, 4, 8, 2>(p, pad, st);
         case C64_128x128: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 2>(p, pad, st);
         case C64S_128x64: return launch_c64_cfg<T, 128, 64, 2, 2, 8, 1>(p, pad, st);
         case C64S_128x128:

@@ -31,6 +31,8 @@ if ROOT not in sys.path:
 PEAK_F16_TFLOPS = 2516.6     # 256 CU x 4096 flop/clk x 2.4 GHz, dense fp16/bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 METRIC = "conv fwd+dgrad+wgrad TFLOP/s on ResNet-50 shapes; % of fp16 MFMA peak"
+METRIC_DW = ("depthwise conv fwd+dgrad+wgrad compulsory HBM GB/s on EfficientNet-B0 shapes; "
+             "% of 8 TB/s")
 
 
 def parse():
@@ -38,7 +40,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "cfg2", "cfg3", "cfg4"])
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "cfg2", "cfg3", "cfg4", "effdw"],
+                    help="sweep: the 53 ResNet-50 layers (the headline metric); effdw: the 16 "
+                         "depthwise layers of EfficientNet-B0 at batch 128 (grouped convolution "
+                         "with one channel per group, reported as HBM GB/s)")
     ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
     ap.add_argument("--batch", type=int, default=0, help="override the batch size")
     ap.add_argument("--cpu-seconds", type=float, default=30.0,
@@ -63,10 +68,12 @@ def parse():
 
 def layers_for(args):
     from paper_2102_06725_amd import inputs as I
-    if args.workload == "sweep":
-        wl = I.workload(5, args.dtype, batch=args.batch or None)
+    if args.workload in ("sweep", "effdw"):
+        cfg = 5 if args.workload == "sweep" else 6
+        wl = I.workload(cfg, args.dtype, batch=args.batch or None)
+        shapes = I.resnet50_layers if cfg == 5 else I.efficientnet_b0_depthwise
         expanded = []
-        for l, c in I.resnet50_layers(wl.layers[0].n):
+        for l, c in shapes(wl.layers[0].n):
             expanded += [l] * c
         if args.layers:
             keep = set(args.layers.split(","))
@@ -94,16 +101,18 @@ class LayerBuffers:
             self.x = torch.empty((L.n, L.h, L.w, L.c), device=dev, dtype=tdt)
         else:
             self.x = self.x_raw
-        std = math.sqrt(2.0 / (cl * L.r * L.s))
-        w = torch.zeros((L.k, L.r, L.s, L.c), device=dev, dtype=torch.float32)
-        w[..., :cl] = torch.randn((L.k, L.r, L.s, cl), generator=g, device=dev) * std
+        # He-normal weights: fan-in is the group's logical channels times R*S
+        cg, cgl = L.c // L.groups, cl // L.groups
+        std = math.sqrt(2.0 / (cgl * L.r * L.s))
+        w = torch.zeros((L.k, L.r, L.s, cg), device=dev, dtype=torch.float32)
+        w[..., :cgl] = torch.randn((L.k, L.r, L.s, cgl), generator=g, device=dev) * std
         self.w = w.to(tdt)
         dy = torch.randn((L.n, L.p, L.q, L.k), generator=g, device=dev) * (wl.loss_scale * wl.dy_std)
         self.dy = dy.to(tdt)
         del x, w, dy
         self.y = torch.empty((L.n, L.p, L.q, L.k), device=dev, dtype=tdt)
         self.dx = torch.empty((L.n, L.h, L.w, L.c), device=dev, dtype=tdt) if L.dgrad else None
-        self.dw = torch.empty((L.k, L.r, L.s, L.c), device=dev, dtype=torch.float32)
+        self.dw = torch.empty((L.k, L.r, L.s, cg), device=dev, dtype=torch.float32)
         self.desc = nc.make_desc(L.n, L.c, L.h, L.w, L.k, L.r, L.s, (L.stride, L.stride),
                                  (L.pad, L.pad), (L.dil, L.dil), L.groups, nc.NNCONV_NHWC,
                                  nc.NNCONV_F16 if wl.dtype == "f16" else nc.NNCONV_BF16)
@@ -440,6 +449,11 @@ def main():
 
     step_flops = sum(L.flops() * (3 if L.dgrad else 2) for L in layers)
     value = step_flops * args.steps / elapsed / 1e12
+    depthwise = args.workload == "effdw"
+    step_bytes = sum(compulsory_bytes(L, p) for L in layers
+                     for p in (("fwd", "dgrad", "wgrad") if L.dgrad else ("fwd", "wgrad")))
+    if depthwise:  # bound by HBM: report the compulsory bytes moved per second
+        value = step_bytes * args.steps / elapsed / 1e9
 
     # per-pass time from the events inside the timed steps
     pass_ms = {"fwd": 0.0, "dgrad": 0.0, "wgrad": 0.0}
@@ -480,6 +494,14 @@ def main():
                     "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS, "traffic": traffic,
                     "avg_launch_us": fwd_avg_ms * 1e3,
                     "avg_flops_per_launch": fwd_avg_flops}
+        if depthwise:
+            fwd_bytes = sum(compulsory_bytes(L, "fwd") for L in layers) / len(layers)
+            gbs = fwd_bytes / (fwd_avg_ms * 1e-3) / 1e9
+            roofline = {"kernel": "dw_fwd_kernel, one launch per nnconv_fwd call",
+                        "bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                        "avg_launch_us": fwd_avg_ms * 1e3,
+                        "avg_bytes_per_launch": fwd_bytes}
 
     update = measure_update(args, layers, torch, nc, dev, sptr, stream) if use_ev else None
 
@@ -492,9 +514,9 @@ def main():
 
     L0 = layers[0]
     out = {
-        "metric": METRIC,
+        "metric": METRIC_DW if depthwise else METRIC,
         "value": value,
-        "unit": "TFLOP/s",
+        "unit": "GB/s" if depthwise else "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -508,8 +530,9 @@ def main():
                                "loss scale %g, fp32 dw" % (args.dtype, wl.loss_scale),
                    "batch": L0.n, "layers": len(layers),
                    "layer_passes": sum(3 if L.dgrad else 2 for L in layers),
-                   "tflop_per_step": step_flops / 1e12},
-        "pct_of_peak": 100.0 * value / PEAK_F16_TFLOPS,
+                   "tflop_per_step": step_flops / 1e12,
+                   "compulsory_gb_per_step": step_bytes / 1e9},
+        "pct_of_peak": 100.0 * value / (PEAK_HBM_GBS if depthwise else PEAK_F16_TFLOPS),
         "per_pass": per_pass,
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -67,6 +67,27 @@ bool fast_shape(const Geom &G) {
     return true;
 }
 
+// Depthwise convolution on its vector-ALU kernels: one input and one output
+// channel per group, 8-channel vectors, square 3x3 / 5x5 / 7x7 filters.
+bool dw_shape(const Geom &G) {
+    if (!(G.g == G.c && G.k == G.c && G.c % 8 == 0 && dw_supported((int)G.r, (int)G.s)))
+        return false;
+    const int64_t lim = MAX_BUFFER_BYTES / 2;
+    return G.n * G.h * G.w * G.c <= lim && G.n * G.p * G.q * G.k <= lim;
+}
+
+// Backward-weight pixel ranges of the depthwise kernel: about 2048
+// workgroups, at least 256 pixels per range.
+int32_t dw_wgrad_splits(const Geom &G) {
+    const int64_t cblocks = (G.c / 8 + 7) / 8;
+    const int64_t npq = G.n * G.p * G.q;
+    int64_t s = 2048 / (cblocks * G.r);
+    if (s > npq / 256) s = npq / 256;
+    if (s > 4096) s = 4096;
+    if (s < 1) s = 1;
+    return (int32_t)s;
+}
+
 // ---------------------------------------------------------------------------
 // planning: workspace regions and split counts (pure functions of the shape)
 // ---------------------------------------------------------------------------
@@ -189,7 +210,36 @@ size_t direct_ws(const Geom &G, nnconv_pass pass) {
     return align256((size_t)plan_wgrad_direct_splits(G) * G.k * G.r * G.s * G.cg * 4);
 }
 
+// Depthwise workspace: the channel-last copies for NCHW calls, fp32 split
+// partials (backward-weight).
+Regions dw_regions(const Geom &G, nnconv_pass pass) {
+    Regions R = {0, 0, 0, 0, 0};
+    const size_t xb = G.n * G.h * G.w * G.c * 2;
+    const size_t yb = G.n * G.p * G.q * G.k * 2;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    const bool nchw = G.layout == NNCONV_NCHW;
+    if (pass == NNCONV_FWD) {
+        if (nchw) { R.a = take(xb); R.c = take(yb); }
+    } else if (pass == NNCONV_DGRAD) {
+        if (nchw) { R.a = take(yb); R.c = take(xb); }
+    } else {
+        if (nchw) { R.a = take(xb); R.b = take(yb); }
+        R.c = take((size_t)dw_wgrad_splits(G) * G.c * G.r * G.s * 4);
+    }
+    R.total = off;
+    return R;
+}
+
 size_t workspace_bytes(const Geom &G, nnconv_pass pass) {
+    if (dw_shape(G)) {  // the vector kernels, or the direct ones for unaligned pointers
+        const size_t a = dw_regions(G, pass).total, b = direct_ws(G, pass);
+        return a > b ? a : b;
+    }
     size_t d = direct_ws(G, pass);
     if (!fast_shape(G)) return d;
     size_t f = fast_regions(G, pass).total;
@@ -510,6 +560,79 @@ nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *pa
     return NNCONV_OK;
 }
 
+DWParams dw_params(const Geom &G, float alpha) {
+    DWParams p;
+    memset(&p, 0, sizeof(p));
+    p.n = (int32_t)G.n; p.c = (int32_t)G.c; p.h = (int32_t)G.h; p.w = (int32_t)G.w;
+    p.p = (int32_t)G.p; p.q = (int32_t)G.q; p.r = (int32_t)G.r; p.s = (int32_t)G.s;
+    p.sh = (int32_t)G.sh; p.sw = (int32_t)G.sw; p.ph = (int32_t)G.ph; p.pw = (int32_t)G.pw;
+    p.dh = (int32_t)G.dh; p.dw = (int32_t)G.dw;
+    p.c8 = (int32_t)(G.c / 8);
+    p.cblocks = (int32_t)((G.c / 8 + 7) / 8);
+    p.x_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+    p.dy_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
+    p.splits = dw_wgrad_splits(G);
+    const int64_t npq = G.n * G.p * G.q;
+    p.pix_per_split = (npq + p.splits - 1) / p.splits;
+    p.alpha = alpha;
+    return p;
+}
+
+// Depthwise passes, either layout.  Every buffer argument is caller-owned
+// device memory; ws is laid out by dw_regions.
+nnconv_status dw_fwd(const Geom &G, const void *x, const void *w, void *y, float alpha, char *ws,
+                     hipStream_t st) {
+    const Regions R = dw_regions(G, NNCONV_FWD);
+    const void *xn = x;
+    void *yn = y;
+    if (G.layout == NNCONV_NCHW) {
+        TRY_HIP(launch_transpose16(x, ws + R.a, G.n, G.c, G.h * G.w, G.c, st));
+        xn = ws + R.a;
+        yn = ws + R.c;
+    }
+    TRY_HIP(launch_depthwise(G.dtype, 0, dw_params(G, alpha), xn, w, yn, st));
+    if (G.layout == NNCONV_NCHW)
+        return hip_status(launch_transpose16(yn, y, G.n, G.p * G.q, G.k, G.p * G.q, st));
+    return NNCONV_OK;
+}
+
+nnconv_status dw_dgrad(const Geom &G, const void *dy, const void *w, void *dx, float alpha,
+                       char *ws, hipStream_t st) {
+    const Regions R = dw_regions(G, NNCONV_DGRAD);
+    const void *dyn = dy;
+    void *dxn = dx;
+    if (G.layout == NNCONV_NCHW) {
+        TRY_HIP(launch_transpose16(dy, ws + R.a, G.n, G.k, G.p * G.q, G.k, st));
+        dyn = ws + R.a;
+        dxn = ws + R.c;
+    }
+    TRY_HIP(launch_depthwise(G.dtype, 1, dw_params(G, alpha), dyn, w, dxn, st));
+    if (G.layout == NNCONV_NCHW)
+        return hip_status(launch_transpose16(dxn, dx, G.n, G.h * G.w, G.c, G.h * G.w, st));
+    return NNCONV_OK;
+}
+
+nnconv_status dw_wgrad(const Geom &G, const void *x, const void *dy, void *dw, int out_code,
+                       float inv_loss_scale, int accumulate, int32_t *flag, char *ws,
+                       hipStream_t st) {
+    const Regions R = dw_regions(G, NNCONV_WGRAD);
+    const void *xn = x, *dyn = dy;
+    if (G.layout == NNCONV_NCHW) {
+        TRY_HIP(launch_transpose16(x, ws + R.a, G.n, G.c, G.h * G.w, G.c, st));
+        TRY_HIP(launch_transpose16(dy, ws + R.b, G.n, G.k, G.p * G.q, G.k, st));
+        xn = ws + R.a;
+        dyn = ws + R.b;
+    }
+    const DWParams p = dw_params(G, 1.0f);
+    float *part = (float *)(ws + R.c);
+    TRY_HIP(launch_depthwise(G.dtype, 2, p, xn, dyn, part, st));
+    // partials are [split][C][R*S]: the [K][R][S][Cg] order with Cg = 1,
+    // which is also [K][Cg][R][S]
+    return hip_status(launch_wgrad_reduce(part, p.splits, G.c * G.r * G.s, dw, out_code,
+                                          inv_loss_scale, accumulate, flag, 0, 1,
+                                          (int32_t)(G.r * G.s), st));
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -571,6 +694,11 @@ NNCONV_API nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, cons
     if ((st = check_ws(G, NNCONV_FWD, ws, ws_bytes)) != NNCONV_OK) return st;
     hipStream_t s = (hipStream_t)hip_stream;
     clear_stale_error();
+    if (dw_shape(G)) {
+        if (!aligned(x, 16) || !aligned(w, 2) || !aligned(y, 16) || !aligned(ws, 16))
+            return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
+        return dw_fwd(G, x, w, y, alpha, (char *)ws, s);
+    }
     const bool fast = fast_shape(G) && aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                       (G.layout == NNCONV_NHWC || aligned(ws, 16));
     if (!fast) return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
@@ -595,6 +723,12 @@ NNCONV_API nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, c
     if ((st = check_ws(G, NNCONV_DGRAD, ws, ws_bytes)) != NNCONV_OK) return st;
     hipStream_t s = (hipStream_t)hip_stream;
     clear_stale_error();
+    if (dw_shape(G)) {
+        if (!aligned(dy, 16) || !aligned(w, 2) || !aligned(dx, 16) || !aligned(ws, 16))
+            return hip_status(
+                launch_direct_dgrad(G.dtype, direct_params(G, alpha), dy, w, dx, s));
+        return dw_dgrad(G, dy, w, dx, alpha, (char *)ws, s);
+    }
     const bool fast = fast_shape(G) && aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
                       aligned(ws, 16);
     if (!fast)
@@ -643,6 +777,9 @@ NNCONV_API nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, co
     const int out_code = dw_dtype == NNCONV_F32 ? 2 : (dw_dtype == NNCONV_F16 ? 0 : 1);
     const int64_t count = G.k * G.r * G.s * G.cg;
     const int kcrs = G.layout == NNCONV_NCHW;
+    if (dw_shape(G) && aligned(x, 16) && aligned(dy, 16) && aligned(ws, 16))
+        return dw_wgrad(G, x, dy, dw, out_code, inv_loss_scale, accumulate, overflow_flag,
+                        (char *)ws, s);
     const bool fast = fast_shape(G) && aligned(x, 16) && aligned(dy, 16) && aligned(ws, 16);
     if (!fast) {
         const int32_t splits = plan_wgrad_direct_splits(G);

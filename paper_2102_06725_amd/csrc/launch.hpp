@@ -170,6 +170,26 @@ hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t
 hipError_t launch_pad_channels16(const void *src, void *dst, int64_t rows, int32_t c,
                                  int32_t c_pad, hipStream_t st);
 
+// Depthwise convolution (groups = C = K), channel-last, C % 8 == 0, square
+// 3x3 / 5x5 / 7x7 filters (depthwise.hip).  Weights are [C][R][S] (the
+// KRSC and KCRS layouts coincide for one channel per group).
+struct DWParams {
+    int32_t n, c, h, w, p, q, r, s;
+    int32_t sh, sw, ph, pw, dh, dw;
+    int32_t c8;              // c / 8
+    int32_t cblocks;         // 64-channel blocks: (c8 + 7) / 8
+    uint32_t x_bytes, dy_bytes;  // x and y / dy sizes (buffer range checks)
+    int32_t splits;          // backward-weight pixel ranges
+    int64_t pix_per_split;
+    float alpha;
+};
+bool dw_supported(int r, int s);
+// pass 0: forward (a = x, b = w, out = y); 1: backward-data (a = dy, b = w,
+// out = dx); 2: backward-weight partials (a = x, b = dy,
+// out = ws[split][c][r*S + s], fp32).
+hipError_t launch_depthwise(int dtype, int pass, const DWParams &p, const void *a, const void *b,
+                            void *out, hipStream_t st);
+
 // Training-step pieces (update.hip).  The state type is the C ABI's.
 hipError_t launch_loss_scaler_init(nnconv_loss_scaler *s, float scale, float factor,
                                    int32_t interval, hipStream_t st);

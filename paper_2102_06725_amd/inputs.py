@@ -161,7 +161,30 @@ def resnet50_layers(batch: int) -> List[Tuple[Layer, int]]:
     return [(l, l.count) for l in L]
 
 
-# The five workloads: shapes, layout, dtype, distributions, loss scale.
+def efficientnet_b0_depthwise(batch: int) -> List[Tuple[Layer, int]]:
+    """The 16 depthwise convolutions of EfficientNet-B0 (224x224 input): the
+    MBConv blocks' k x k depthwise stage, one group per channel, with the
+    expanded channel counts, the stride on each stage's first block and
+    "same" padding k // 2.  Distinct shapes with their multiplicities."""
+    L = []
+    def add(name, c, h, k, stride, count):
+        L.append(Layer(name, batch, c, h, h, c, k, k, stride, k // 2, groups=c, count=count))
+    add("mb1_dw3", 32, 112, 3, 1, 1)
+    add("mb2a_dw3", 96, 112, 3, 2, 1)
+    add("mb2b_dw3", 144, 56, 3, 1, 1)
+    add("mb3a_dw5", 144, 56, 5, 2, 1)
+    add("mb3b_dw5", 240, 28, 5, 1, 1)
+    add("mb4a_dw3", 240, 28, 3, 2, 1)
+    add("mb4b_dw3", 480, 14, 3, 1, 2)
+    add("mb5a_dw5", 480, 14, 5, 1, 1)
+    add("mb5b_dw5", 672, 14, 5, 1, 2)
+    add("mb6a_dw5", 672, 14, 5, 2, 1)
+    add("mb6b_dw5", 1152, 7, 5, 1, 3)
+    add("mb7_dw3", 1152, 7, 3, 1, 1)
+    return [(l, l.count) for l in L]
+
+
+# The workloads: shapes, layout, dtype, distributions, loss scale.
 @dataclasses.dataclass(frozen=True)
 class Workload:
     name: str
@@ -179,7 +202,8 @@ class Workload:
 def workload(cfg: int, dtype: str = F16, batch: int | None = None) -> Workload:
     """Config 1: tiny 3x3 NCHW; 2: ResNet-50 stage-1 bottleneck at batch 64;
     3: stage transitions at batch 128; 4: stem at batch 128; 5: all 53 layers
-    at batch 256."""
+    at batch 256; 6: the depthwise layers of EfficientNet-B0 at batch 128
+    (grouped convolution with one channel per group)."""
     if cfg == 1:
         n = batch or 2
         s = 1.0 / math.sqrt(16 * 9)
@@ -210,7 +234,12 @@ def workload(cfg: int, dtype: str = F16, batch: int | None = None) -> Workload:
         ls = tuple(l for l, _ in resnet50_layers(n))
         return Workload("ResNet-50 all 53 conv layers batch %d" % n, ls, "nhwc", dtype,
                         1024.0, "absnormal", 1.0, "he", 1e-3)
-    raise ValueError("config must be 1..5")
+    if cfg == 6:
+        n = batch or 128
+        ls = tuple(l for l, _ in efficientnet_b0_depthwise(n))
+        return Workload("EfficientNet-B0 16 depthwise layers batch %d" % n, ls, "nhwc", dtype,
+                        1024.0, "absnormal", 1.0, "he", 1e-3)
+    raise ValueError("config must be 1..6")
 
 
 def layer_tensors(wl: Workload, li: int, cfg: int, layer: Layer | None = None):

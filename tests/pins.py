@@ -108,6 +108,36 @@ def pin_scipy_correlate(lib):
         _close(cv.fwd(x, wt)[0, 0], ref, what="correlate2d")
 
 
+def pin_depthwise_correlate(lib):
+    """Depthwise (groups = C = K): every output channel is the single-channel
+    cross-correlation of its own input channel with its own filter
+    (scipy.signal.correlate2d on the zero-padded image), subsampled by the
+    stride; dgrad and wgrad follow from the adjoint identities per channel."""
+    from scipy.signal import correlate2d
+    rng = np.random.default_rng(17)
+    for (n, c, h, w, r, st, pd) in [(2, 3, 7, 6, 3, 1, 1), (1, 4, 9, 8, 5, 2, 2),
+                                    (2, 2, 6, 7, 3, 2, 0)]:
+        x = rng.standard_normal((n, c, h, w))
+        wt = rng.standard_normal((c, 1, r, r))
+        cv = orc.Conv(n, c, h, w, c, r, r, (st, st), (pd, pd), (1, 1), c, lib=lib)
+        y = cv.fwd(x, wt)
+        ref = np.empty_like(y)
+        for b in range(n):
+            for ch in range(c):
+                xp = np.pad(x[b, ch], ((pd, pd), (pd, pd)))
+                ref[b, ch] = correlate2d(xp, wt[ch, 0], mode="valid")[::st, ::st]
+        _close(y, ref, what="depthwise correlate2d")
+        dy = rng.standard_normal(y.shape)
+        dx = cv.dgrad(dy, wt)
+        dw = cv.wgrad(x, dy)
+        for ch in range(c):
+            one = orc.Conv(n, 1, h, w, 1, r, r, (st, st), (pd, pd), (1, 1), 1, lib=lib)
+            _close(dx[:, ch:ch + 1], one.dgrad(dy[:, ch:ch + 1], wt[ch:ch + 1]),
+                   what="depthwise dgrad per channel")
+            _close(dw[ch:ch + 1], one.wgrad(x[:, ch:ch + 1], dy[:, ch:ch + 1]),
+                   what="depthwise wgrad per channel")
+
+
 def pin_matmul_1x1(lib):
     """1x1 kernel, stride 1, no padding: Y = W X per pixel, DX = W^T DY,
     DW = sum over pixels of DY X^T (numpy matmul)."""
@@ -395,8 +425,8 @@ def pin_points(lib):
         assert np.array_equal(cv.wgrad_points(x, dy, np.arange(dw.size)), dw.ravel())
 
 
-ALL_PINS = [pin_torch, pin_scipy_correlate, pin_matmul_1x1, pin_delta_kernel,
-            pin_ones_closed_form, pin_output_dims, pin_handworked, pin_adjoint,
+ALL_PINS = [pin_torch, pin_scipy_correlate, pin_depthwise_correlate, pin_matmul_1x1,
+            pin_delta_kernel, pin_ones_closed_form, pin_output_dims, pin_handworked, pin_adjoint,
             pin_gather_scatter, pin_groups_concat, pin_dilation_zero_insert,
             pin_stride_subsample, pin_linearity, pin_loss_scale, pin_nonfinite,
             pin_points]

@@ -83,6 +83,20 @@ SMALL = [
     ("3x3 C256 K512 bf16", Case(L("s8", 2, 256, 6, 5, 512, 3, 3, 1, 1), dtype=I.BF16)),
     ("P = Q = 1", Case(L("s", 2, 16, 3, 3, 16, 3, 3, 1, 0))),
     ("H = W = 1, 1x1", Case(L("t", 5, 32, 1, 1, 24, 1, 1))),
+    # depthwise (groups = C = K) on the vector-ALU kernels
+    ("depthwise 3x3", Case(L("dw1", 3, 64, 13, 11, 64, 3, 3, 1, 1, groups=64))),
+    ("depthwise 3x3 stride 2", Case(L("dw2", 2, 96, 15, 14, 96, 3, 3, 2, 1, groups=96))),
+    ("depthwise 5x5 stride 2 bf16", Case(L("dw3", 2, 40, 17, 16, 40, 5, 5, 2, 2, groups=40),
+                                         dtype=I.BF16)),
+    ("depthwise 7x7 dilation 2", Case(L("dw4", 2, 16, 20, 19, 16, 7, 7, 1, 6, dil=2,
+                                        groups=16))),
+    ("depthwise 3x3 NCHW", Case(L("dw5", 2, 24, 9, 10, 24, 3, 3, 1, 1, groups=24),
+                                layout="nchw")),
+    ("depthwise 3x3 pad 0 C320", Case(L("dw6", 2, 320, 9, 8, 320, 3, 3, 1, 0, groups=320))),
+    ("depthwise 5x5 stride 3 ragged", Case(L("dw7", 3, 8, 11, 13, 8, 5, 5, 3, 1, groups=8))),
+    ("depthwise 3x3 H = W = 1", Case(L("dw8", 4, 32, 1, 1, 32, 3, 3, 1, 1, groups=32))),
+    ("direct: depthwise C12", Case(L("dw9", 2, 12, 9, 9, 12, 3, 3, 1, 1, groups=12))),
+    ("direct: depthwise 3x5", Case(L("dw10", 2, 16, 8, 9, 16, 3, 5, 1, 1, groups=16))),
 ]
 
 
@@ -104,6 +118,25 @@ def test_deterministic():
     b = run_gpu(case, t)
     for k in ("y_bits", "dx_bits", "dw_bits"):
         assert np.array_equal(a[k], b[k]), k
+
+
+def test_depthwise_deterministic_and_loss_scale_invariant():
+    """The depthwise kernels sum in a fixed order: two runs agree bitwise,
+    and wgrad(x, S*dy)/S == wgrad(x, dy) bitwise for S = 1024."""
+    base = Case(L("dwi", 4, 64, 20, 18, 64, 3, 3, 1, 1, groups=64), loss_scale=1.0,
+                dy_std=1.0)
+    t1 = base.tensors()
+    a = run_gpu(base, t1)
+    b = run_gpu(base, t1)
+    for k in ("y_bits", "dx_bits", "dw_bits"):
+        assert np.array_equal(a[k], b[k]), k
+    dy1 = I.from_bits(t1["dy"], I.F16)
+    tS = dict(t1)
+    tS["dy"] = I.to_bits(dy1 * 1024.0, I.F16)
+    assert np.array_equal(I.from_bits(tS["dy"], I.F16), dy1 * 1024.0)
+    r1 = run_gpu(base, t1, passes=("wgrad",), inv_scale=1.0)
+    rS = run_gpu(base, tS, passes=("wgrad",), inv_scale=1.0 / 1024.0)
+    assert np.array_equal(r1["dw_bits"], rS["dw_bits"])
 
 
 def test_loss_scale_power_of_two_invariant():

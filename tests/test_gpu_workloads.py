@@ -1,8 +1,9 @@
 """Workload parity at full size.
 
 Each seeded workload (the stage-1 bottleneck at batch 64, the stage
-transitions at batch 128, the stem at batch 128, and every distinct layer of
-the 53-layer ResNet-50 sweep at batch 256) runs through the same library
+transitions at batch 128, the stem at batch 128, every distinct layer of
+the 53-layer ResNet-50 sweep at batch 256, and the depthwise layers of
+EfficientNet-B0 at batch 128) runs through the same library
 calls, descriptors and therefore the same kernel launches that bench.py
 times.  The oracle's single-point routines then evaluate sampled outputs:
 65,536 random positions of y and of dx, every border pixel (all channels) of
@@ -11,8 +12,8 @@ first and last filter in full.  The error is max|err| / max|ref| over the
 sampled positions.  Every output element is also checked for bitwise
 reproducibility across two runs.
 
-Every distinct sweep layer also runs at batch 3 (ragged tiles) against the
-full oracle, in fp16 and bf16."""
+Every distinct sweep layer and depthwise layer also runs at batch 3
+(ragged tiles) against the full oracle, in fp16 and bf16."""
 import zlib
 
 import numpy as np
@@ -48,7 +49,8 @@ def workload_cases(cfg, dtype=I.F16):
     return out
 
 
-FULL_SIZE = workload_cases(2) + workload_cases(3) + workload_cases(4) + workload_cases(5)
+FULL_SIZE = (workload_cases(2) + workload_cases(3) + workload_cases(4) + workload_cases(5) +
+             workload_cases(6))
 
 
 def border_and_random(rng, shape, n_random):
@@ -156,6 +158,13 @@ SWEEP_B3 = [("%s %s b3" % (L.name, dt),
                   layer_id=li))
             for dt in (I.F16, I.BF16)
             for li, (L, _) in enumerate(I.resnet50_layers(3))]
+
+
+SWEEP_B3 += [("%s %s b3" % (L.name, dt),
+              Case(L.with_batch(3), layout="nhwc", dtype=dt, loss_scale=1024.0,
+                   x_kind="absnormal", dy_std=1e-3, cfg=6, layer_id=li))
+             for dt in (I.F16, I.BF16)
+             for li, (L, _) in enumerate(I.efficientnet_b0_depthwise(3))]
 
 
 @pytest.mark.parametrize("name,case", SWEEP_B3, ids=[c[0] for c in SWEEP_B3])

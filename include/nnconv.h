@@ -35,6 +35,12 @@
  *   - Fast (matrix-core) paths need 16-byte aligned pointers and Cg, Kg that
  *     are multiples of 8; other valid shapes run on slower direct kernels
  *     with identical semantics.
+ *   - Depthwise convolution (groups == c == k, one channel per group, the
+ *     MobileNet / EfficientNet layers trained with the paper's framework)
+ *     with c a multiple of 8, a square 3x3, 5x5 or 7x7 filter and 16-byte
+ *     aligned activations runs on dedicated vector-ALU kernels (the pass is
+ *     bound by memory, not by arithmetic); w and dw are [K][R][S] in both
+ *     layouts (one channel per filter).
  *
  * Errors: every argument check happens on the host before anything is
  * queued.  On a non-OK status nothing is launched and no output or

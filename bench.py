@@ -205,11 +205,11 @@ def stored_traffic():
 def is_forward_launch(names, i):
     """In this script's launch order (flag clear, then per layer: optional
     stem channel padding, forward, backward-data kernels, backward-weight
-    kernel and its reduction) a forward launch is an implicit-GEMM or stem
-    dispatch that follows a non-library dispatch, a split reduction or a
-    padding copy."""
+    kernel and its reduction) a forward launch is an implicit-GEMM, stem or
+    depthwise-forward dispatch that follows a non-library dispatch, a split
+    reduction or a padding copy."""
     n = names[i]
-    if "nnconv::" not in n or not ("igemm" in n or "stem_fwd" in n):
+    if "nnconv::" not in n or not ("igemm" in n or "stem_fwd" in n or "dw_fwd" in n):
         return False
     if i == 0:
         return True

@@ -33,6 +33,8 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "conv fwd+dgrad+wgrad TFLOP/s on ResNet-50 shapes; % of fp16 MFMA peak"
 METRIC_DW = ("depthwise conv fwd+dgrad+wgrad compulsory HBM GB/s on EfficientNet-B0 shapes; "
              "% of 8 TB/s")
+METRIC_RNXT = ("grouped conv fwd+dgrad+wgrad algorithmic TFLOP/s on ResNeXt-50 32x4d shapes; "
+               "% of fp16 MFMA peak")
 
 
 def parse():
@@ -40,10 +42,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "cfg2", "cfg3", "cfg4", "effdw"],
+    ap.add_argument("--workload", default="sweep",
+                    choices=["sweep", "cfg2", "cfg3", "cfg4", "effdw", "rnxt"],
                     help="sweep: the 53 ResNet-50 layers (the headline metric); effdw: the 16 "
-                         "depthwise layers of EfficientNet-B0 at batch 128 (grouped convolution "
-                         "with one channel per group, reported as HBM GB/s)")
+                         "depthwise layers of EfficientNet-B0 at batch 128 (one channel per "
+                         "group, reported as HBM GB/s); rnxt: the 16 grouped 3x3 layers of "
+                         "ResNeXt-50 32x4d at batch 128 (algorithmic TFLOP/s)")
     ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
     ap.add_argument("--batch", type=int, default=0, help="override the batch size")
     ap.add_argument("--cpu-seconds", type=float, default=30.0,
@@ -68,10 +72,11 @@ def parse():
 
 def layers_for(args):
     from paper_2102_06725_amd import inputs as I
-    if args.workload in ("sweep", "effdw"):
-        cfg = 5 if args.workload == "sweep" else 6
+    if args.workload in ("sweep", "effdw", "rnxt"):
+        cfg = {"sweep": 5, "effdw": 6, "rnxt": 7}[args.workload]
         wl = I.workload(cfg, args.dtype, batch=args.batch or None)
-        shapes = I.resnet50_layers if cfg == 5 else I.efficientnet_b0_depthwise
+        shapes = {5: I.resnet50_layers, 6: I.efficientnet_b0_depthwise,
+                  7: I.resnext50_grouped}[cfg]
         expanded = []
         for l, c in shapes(wl.layers[0].n):
             expanded += [l] * c
@@ -514,7 +519,7 @@ def main():
 
     L0 = layers[0]
     out = {
-        "metric": METRIC_DW if depthwise else METRIC,
+        "metric": METRIC_DW if depthwise else METRIC_RNXT if args.workload == "rnxt" else METRIC,
         "value": value,
         "unit": "GB/s" if depthwise else "TFLOP/s",
         "n_gpus": 1,

@@ -88,6 +88,31 @@ int32_t dw_wgrad_splits(const Geom &G) {
     return (int32_t)s;
 }
 
+// Grouped convolution with m = Cg = Kg channels per group, m < 64 dividing 64
+// (ResNeXt's g = 32 layers: m = 4-32): run as super-groups of 64 channels
+// with block-diagonal weights on the 64-channel-slice kernels.  For finite
+// inputs the sums are the same products plus exact zeros; a non-finite input
+// can turn the other groups of its super-group into NaN (0 * inf).
+constexpr int64_t SUPER_GROUP = 64;
+
+bool fast_shape(const Geom &G);
+
+bool sg_shape(const Geom &G) {
+    if (G.g < 2 || G.cg != G.kg || G.cg >= SUPER_GROUP || SUPER_GROUP % G.cg != 0 ||
+        G.c % SUPER_GROUP != 0)
+        return false;
+    if (dw_shape(G)) return false;  // depthwise has its own kernels
+    return true;
+}
+
+// The same convolution with groups of SUPER_GROUP channels.
+Geom sg_geom(const Geom &G) {
+    Geom S = G;
+    S.g = G.c / SUPER_GROUP;
+    S.cg = S.kg = SUPER_GROUP;
+    return S;
+}
+
 // ---------------------------------------------------------------------------
 // planning: workspace regions and split counts (pure functions of the shape)
 // ---------------------------------------------------------------------------
@@ -235,7 +260,26 @@ Regions dw_regions(const Geom &G, nnconv_pass pass) {
     return R;
 }
 
+// Super-group workspace: the block-diagonal weights [K][R][S][64] (forward,
+// backward-data), then the super-grouped problem's own regions.
+Regions sg_regions(const Geom &G, nnconv_pass pass) {
+    const Geom S = sg_geom(G);
+    Regions R = {0, 0, 0, 0, 0};
+    const size_t wexp = pass == NNCONV_WGRAD ? 0 : align256(G.k * G.r * G.s * SUPER_GROUP * 2);
+    const Regions in = fast_regions(S, pass);
+    R.d = 0;            // expanded weights
+    R.a = wexp + in.a;  // NCHW copies / dgrad weight re-layout / partials, shifted
+    R.b = wexp + in.b;
+    R.c = wexp + in.c;
+    R.total = wexp + in.total;
+    return R;
+}
+
 size_t workspace_bytes(const Geom &G, nnconv_pass pass) {
+    if (sg_shape(G) && fast_shape(sg_geom(G))) {  // or the direct kernels (unaligned)
+        const size_t a = sg_regions(G, pass).total, b = direct_ws(G, pass);
+        return a > b ? a : b;
+    }
     if (dw_shape(G)) {  // the vector kernels, or the direct ones for unaligned pointers
         const size_t a = dw_regions(G, pass).total, b = direct_ws(G, pass);
         return a > b ? a : b;
@@ -633,6 +677,61 @@ nnconv_status dw_wgrad(const Geom &G, const void *x, const void *dy, void *dw, i
                                           (int32_t)(G.r * G.s), st));
 }
 
+nnconv_status sg_fwd(const Geom &G, const void *x, const void *w, void *y, float alpha,
+                     char *ws, hipStream_t st) {
+    const Geom S = sg_geom(G);
+    const Regions R = sg_regions(G, NNCONV_FWD);
+    void *wexp = ws + R.d;
+    TRY_HIP(launch_expand_group_weights(w, wexp, G.k, (int32_t)(G.r * G.s), (int32_t)G.cg,
+                                        (int32_t)SUPER_GROUP, G.layout == NNCONV_NCHW, st));
+    if (G.layout == NNCONV_NHWC) return fwd_fast(S, x, wexp, y, alpha, st);
+    void *xt = ws + R.a, *yt = ws + R.c;
+    TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, st));
+    nnconv_status s = fwd_fast(S, xt, wexp, yt, alpha, st);
+    if (s != NNCONV_OK) return s;
+    return hip_status(launch_transpose16(yt, y, G.n, G.p * G.q, G.k, G.p * G.q, st));
+}
+
+nnconv_status sg_dgrad(const Geom &G, const void *dy, const void *w, void *dx, float alpha,
+                       char *ws, hipStream_t st) {
+    const Geom S = sg_geom(G);
+    const Regions R = sg_regions(G, NNCONV_DGRAD);
+    void *wexp = ws + R.d, *wt = ws + R.b;
+    TRY_HIP(launch_expand_group_weights(w, wexp, G.k, (int32_t)(G.r * G.s), (int32_t)G.cg,
+                                        (int32_t)SUPER_GROUP, G.layout == NNCONV_NCHW, st));
+    // [g][Kg][R*S*Cg] -> [g][R*S*Cg][Kg] for the super-groups
+    TRY_HIP(launch_transpose16(wexp, wt, S.g, S.kg, S.r * S.s * S.cg, S.kg, st));
+    if (G.layout == NNCONV_NHWC) return dgrad_fast(S, dy, wt, dx, alpha, st);
+    void *dyt = ws + R.a, *dxt = ws + R.c;
+    TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, st));
+    nnconv_status s = dgrad_fast(S, dyt, wt, dxt, alpha, st);
+    if (s != NNCONV_OK) return s;
+    return hip_status(launch_transpose16(dxt, dx, G.n, G.h * G.w, G.c, G.h * G.w, st));
+}
+
+nnconv_status sg_wgrad(const Geom &G, const void *x, const void *dy, void *dw, int out_code,
+                       float inv_loss_scale, int accumulate, int32_t *flag, char *ws,
+                       hipStream_t st) {
+    const Geom S = sg_geom(G);
+    const Regions R = sg_regions(G, NNCONV_WGRAD);
+    const void *xn = x, *dyn = dy;
+    if (G.layout == NNCONV_NCHW) {
+        void *xt = ws + R.a, *dyt = ws + R.b;
+        TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, st));
+        TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, st));
+        xn = xt;
+        dyn = dyt;
+    }
+    float *part = (float *)(ws + R.c);
+    nnconv_status s = wgrad_fast(S, xn, dyn, part, st);
+    if (s != NNCONV_OK) return s;
+    const WgPlan pl = plan_wgrad_fast(S);
+    return hip_status(launch_wgrad_reduce_diag(part, pl.splits, G.k, (int32_t)(G.r * G.s),
+                                               (int32_t)G.cg, (int32_t)SUPER_GROUP, dw, out_code,
+                                               inv_loss_scale, accumulate, flag,
+                                               G.layout == NNCONV_NCHW, st));
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -699,6 +798,9 @@ NNCONV_API nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, cons
             return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
         return dw_fwd(G, x, w, y, alpha, (char *)ws, s);
     }
+    if (sg_shape(G) && fast_shape(sg_geom(G)) && aligned(x, 16) && aligned(y, 16) &&
+        aligned(ws, 16))
+        return sg_fwd(G, x, w, y, alpha, (char *)ws, s);
     const bool fast = fast_shape(G) && aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                       (G.layout == NNCONV_NHWC || aligned(ws, 16));
     if (!fast) return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
@@ -729,6 +831,9 @@ NNCONV_API nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, c
                 launch_direct_dgrad(G.dtype, direct_params(G, alpha), dy, w, dx, s));
         return dw_dgrad(G, dy, w, dx, alpha, (char *)ws, s);
     }
+    if (sg_shape(G) && fast_shape(sg_geom(G)) && aligned(dy, 16) && aligned(dx, 16) &&
+        aligned(ws, 16))
+        return sg_dgrad(G, dy, w, dx, alpha, (char *)ws, s);
     const bool fast = fast_shape(G) && aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
                       aligned(ws, 16);
     if (!fast)
@@ -779,6 +884,10 @@ NNCONV_API nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, co
     const int kcrs = G.layout == NNCONV_NCHW;
     if (dw_shape(G) && aligned(x, 16) && aligned(dy, 16) && aligned(ws, 16))
         return dw_wgrad(G, x, dy, dw, out_code, inv_loss_scale, accumulate, overflow_flag,
+                        (char *)ws, s);
+    if (sg_shape(G) && fast_shape(sg_geom(G)) && aligned(x, 16) && aligned(dy, 16) &&
+        aligned(ws, 16))
+        return sg_wgrad(G, x, dy, dw, out_code, inv_loss_scale, accumulate, overflow_flag,
                         (char *)ws, s);
     const bool fast = fast_shape(G) && aligned(x, 16) && aligned(dy, 16) && aligned(ws, 16);
     if (!fast) {

@@ -225,6 +225,40 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
     }
 }
 
+// Block-diagonal super-group weights: dst[k][t][c'] (c' < sg, t < rs) is
+// w[k][c' - base][t] when c' lies in output channel k's own group of m
+// channels (base = ((k % sg) / m) * m), else 0.  src is [K][rs][m] (kcrs = 0)
+// or [K][m][rs] (kcrs = 1).
+__global__ __launch_bounds__(256) void expand_group_weights_kernel(
+    const uint16_t *__restrict__ src, uint16_t *__restrict__ dst, int64_t count, int32_t rs,
+    int32_t m, int32_t sg, int kcrs) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= count) return;
+    const int64_t per_k = (int64_t)rs * sg;
+    const int64_t k = e / per_k;
+    const int64_t rem = e - k * per_k;
+    const int64_t t = rem / sg;
+    const int64_t cp = rem - t * sg;
+    const int64_t base = ((k % sg) / m) * m;
+    uint16_t v = 0;
+    if (cp >= base && cp < base + m) {
+        const int64_t c = cp - base;
+        v = kcrs ? src[(k * m + c) * rs + t] : src[(k * rs + t) * m + c];
+    }
+    dst[e] = v;
+}
+
+hipError_t launch_expand_group_weights(const void *src, void *dst, int64_t k, int32_t rs, int32_t m,
+                                       int32_t sg, int kcrs, hipStream_t st) {
+    const int64_t count = k * rs * sg;
+    if (count <= 0) return hipSuccess;
+    const int64_t nb = (count + 255) / 256;
+    if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(expand_group_weights_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
+                       (const uint16_t *)src, (uint16_t *)dst, count, rs, m, sg, kcrs);
+    return hipGetLastError();
+}
+
 hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
                               int64_t cols, int64_t dst_ld, hipStream_t st) {
     const int64_t tiles_c = (cols + 63) / 64, tiles_r = (dst_ld + 63) / 64;

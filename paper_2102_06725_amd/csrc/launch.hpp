@@ -163,6 +163,20 @@ hipError_t launch_direct_dgrad(int dtype, const DirectParams &p, const void *dy,
 hipError_t launch_direct_wgrad(int dtype, const DirectParams &p, const void *x, const void *dy,
                                float *ws, int32_t splits, hipStream_t st);
 
+// Grouped convolution as super-groups of sg channels (block-diagonal
+// weights).  dst[k][t][c'] = w[k][c' - base][t] inside output channel k's
+// own group of m channels (base = ((k % sg) / m) * m), else 0; src is
+// [K][rs][m] (kcrs = 0) or [K][m][rs] (kcrs = 1).
+hipError_t launch_expand_group_weights(const void *src, void *dst, int64_t k, int32_t rs, int32_t m,
+                                       int32_t sg, int kcrs, hipStream_t st);
+// dw[k][t][c] (c < m; [K][m][R][S] when kcrs) = (accumulate ? dw : 0) +
+// inv_scale * sum_s ws[s][k][t][((k % sg) / m) * m + c]: the diagonal blocks
+// of the super-group weight-gradient partials.
+hipError_t launch_wgrad_reduce_diag(const float *ws, int32_t splits, int64_t k, int32_t rs,
+                                    int32_t m, int32_t sg, void *dw, int out_dtype,
+                                    float inv_scale, int accumulate, int32_t *flag, int kcrs,
+                                    hipStream_t st);
+
 // dst[b][cc][rr] = rr < rows ? src[b][rr][cc] : 0   for rr < dst_ld, cc < cols
 hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
                               int64_t cols, int64_t dst_ld, hipStream_t st);

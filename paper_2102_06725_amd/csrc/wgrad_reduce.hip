@@ -140,6 +140,47 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *__restri
     if (reduce_store<OUT>(sum, t, dw, inv_scale, accumulate, kcrs, cg, rs) && flag) *flag = 1;
 }
 
+// Grouped convolution run as super-groups of SG channels with block-diagonal
+// weights: the partials hold the whole [K][R*S][SG] super-group gradient;
+// this keeps only each output channel's own group (m channels starting at
+// ((k % SG) / m) * m) and finishes it like the other reductions.  One final
+// element (in [K][R][S][m] order) per thread, splits in increasing order.
+template <int OUT>
+__global__ __launch_bounds__(256) void wgrad_reduce_diag_kernel(
+    const float *__restrict__ ws, int32_t splits, int64_t count, int64_t pcount, int32_t rs,
+    int32_t m, int32_t sg, void *dw, float inv_scale, int accumulate, int32_t *flag, int kcrs) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= count) return;
+    const int64_t per_k = (int64_t)rs * m;
+    const int64_t k = e / per_k;
+    const int64_t rem = e - k * per_k;
+    const int64_t tap = rem / m;
+    const int64_t c = rem - tap * m;
+    const int64_t pe = k * rs * sg + tap * sg + ((k % sg) / m) * m + c;
+    float sum = 0.f;
+    for (int sp = 0; sp < splits; ++sp) sum += ws[(int64_t)sp * pcount + pe];
+    if (reduce_store<OUT>(sum, e, dw, inv_scale, accumulate, kcrs, m, rs) && flag) *flag = 1;
+}
+
+hipError_t launch_wgrad_reduce_diag(const float *ws, int32_t splits, int64_t k, int32_t rs,
+                                    int32_t m, int32_t sg, void *dw, int out_dtype,
+                                    float inv_scale, int accumulate, int32_t *flag, int kcrs,
+                                    hipStream_t st) {
+    const int64_t count = k * rs * m, pcount = k * rs * sg;
+    if (count <= 0) return hipSuccess;
+    const int64_t nb = (count + 255) / 256;
+    if (out_dtype == 2)
+        hipLaunchKernelGGL((wgrad_reduce_diag_kernel<2>), dim3((uint32_t)nb), dim3(256), 0, st, ws,
+                           splits, count, pcount, rs, m, sg, dw, inv_scale, accumulate, flag, kcrs);
+    else if (out_dtype == 0)
+        hipLaunchKernelGGL((wgrad_reduce_diag_kernel<0>), dim3((uint32_t)nb), dim3(256), 0, st, ws,
+                           splits, count, pcount, rs, m, sg, dw, inv_scale, accumulate, flag, kcrs);
+    else
+        hipLaunchKernelGGL((wgrad_reduce_diag_kernel<1>), dim3((uint32_t)nb), dim3(256), 0, st, ws,
+                           splits, count, pcount, rs, m, sg, dw, inv_scale, accumulate, flag, kcrs);
+    return hipGetLastError();
+}
+
 template <int OUT, int L>
 static void launch_reduce_vec(const float *ws, int32_t splits, int64_t count, void *dw,
                               float inv_scale, int accumulate, int32_t *flag, int kcrs,

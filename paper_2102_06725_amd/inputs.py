@@ -184,6 +184,24 @@ def efficientnet_b0_depthwise(batch: int) -> List[Tuple[Layer, int]]:
     return [(l, l.count) for l in L]
 
 
+def resnext50_grouped(batch: int) -> List[Tuple[Layer, int]]:
+    """The 16 grouped 3x3 convolutions of ResNeXt-50 (32x4d) at 224x224: 32
+    groups of 4, 8, 16 and 32 channels in the four stages, the stride on the
+    3x3 of each down-sampling block (as in ResNet-50 v1.5).  Distinct shapes
+    with their multiplicities."""
+    L = []
+    def add(name, c, h, stride, count):
+        L.append(Layer(name, batch, c, h, h, c, 3, 3, stride, 1, groups=32, count=count))
+    add("x2_g4", 128, 56, 1, 3)
+    add("x3a_g8", 256, 56, 2, 1)
+    add("x3b_g8", 256, 28, 1, 3)
+    add("x4a_g16", 512, 28, 2, 1)
+    add("x4b_g16", 512, 14, 1, 5)
+    add("x5a_g32", 1024, 14, 2, 1)
+    add("x5b_g32", 1024, 7, 1, 2)
+    return [(l, l.count) for l in L]
+
+
 # The workloads: shapes, layout, dtype, distributions, loss scale.
 @dataclasses.dataclass(frozen=True)
 class Workload:
@@ -203,7 +221,8 @@ def workload(cfg: int, dtype: str = F16, batch: int | None = None) -> Workload:
     """Config 1: tiny 3x3 NCHW; 2: ResNet-50 stage-1 bottleneck at batch 64;
     3: stage transitions at batch 128; 4: stem at batch 128; 5: all 53 layers
     at batch 256; 6: the depthwise layers of EfficientNet-B0 at batch 128
-    (grouped convolution with one channel per group)."""
+    (grouped convolution with one channel per group); 7: the grouped 3x3
+    layers of ResNeXt-50 32x4d at batch 128."""
     if cfg == 1:
         n = batch or 2
         s = 1.0 / math.sqrt(16 * 9)
@@ -239,7 +258,12 @@ def workload(cfg: int, dtype: str = F16, batch: int | None = None) -> Workload:
         ls = tuple(l for l, _ in efficientnet_b0_depthwise(n))
         return Workload("EfficientNet-B0 16 depthwise layers batch %d" % n, ls, "nhwc", dtype,
                         1024.0, "absnormal", 1.0, "he", 1e-3)
-    raise ValueError("config must be 1..6")
+    if cfg == 7:
+        n = batch or 128
+        ls = tuple(l for l, _ in resnext50_grouped(n))
+        return Workload("ResNeXt-50 32x4d 16 grouped 3x3 layers batch %d" % n, ls, "nhwc", dtype,
+                        1024.0, "absnormal", 1.0, "he", 1e-3)
+    raise ValueError("config must be 1..7")
 
 
 def layer_tensors(wl: Workload, li: int, cfg: int, layer: Layer | None = None):

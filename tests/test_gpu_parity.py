@@ -96,6 +96,18 @@ SMALL = [
     ("depthwise 5x5 stride 3 ragged", Case(L("dw7", 3, 8, 11, 13, 8, 5, 5, 3, 1, groups=8))),
     ("depthwise 3x3 H = W = 1", Case(L("dw8", 4, 32, 1, 1, 32, 3, 3, 1, 1, groups=32))),
     ("direct: depthwise C12", Case(L("dw9", 2, 12, 9, 9, 12, 3, 3, 1, 1, groups=12))),
+    # small groups (Cg = Kg < 64) as 64-channel super-groups
+    ("groups 32 x 4 channels", Case(L("sg4", 2, 128, 9, 10, 128, 3, 3, 1, 1, groups=32))),
+    ("groups 32 x 8 channels stride 2", Case(L("sg8", 2, 256, 9, 8, 256, 3, 3, 2, 1,
+                                                 groups=32))),
+    ("groups 8 x 16 channels NCHW", Case(L("sg16", 2, 128, 7, 9, 128, 3, 3, 1, 1, groups=8),
+                                         layout="nchw")),
+    ("groups 4 x 32 channels bf16", Case(L("sg32", 2, 128, 6, 7, 128, 3, 3, 1, 1, groups=4),
+                                         dtype=I.BF16)),
+    ("groups 32 x 2 channels 1x1", Case(L("sg2", 3, 64, 5, 6, 64, 1, 1, groups=32))),
+    ("groups 32 x 4 channels stride 3", Case(L("sg4s3", 2, 128, 10, 11, 128, 3, 3, 3, 1,
+                                                groups=32))),
+    ("depthwise 3x5 as super-groups", Case(L("sg1", 2, 64, 7, 8, 64, 3, 5, 1, 1, groups=64))),
     ("direct: depthwise 3x5", Case(L("dw10", 2, 16, 8, 9, 16, 3, 5, 1, 1, groups=16))),
 ]
 
@@ -134,6 +146,24 @@ def test_depthwise_deterministic_and_loss_scale_invariant():
     tS = dict(t1)
     tS["dy"] = I.to_bits(dy1 * 1024.0, I.F16)
     assert np.array_equal(I.from_bits(tS["dy"], I.F16), dy1 * 1024.0)
+    r1 = run_gpu(base, t1, passes=("wgrad",), inv_scale=1.0)
+    rS = run_gpu(base, tS, passes=("wgrad",), inv_scale=1.0 / 1024.0)
+    assert np.array_equal(r1["dw_bits"], rS["dw_bits"])
+
+
+def test_grouped_deterministic_and_loss_scale_invariant():
+    """Super-grouped small groups: two runs agree bitwise, and the weight
+    gradient keeps the power-of-two loss-scale invariant bitwise."""
+    base = Case(L("sgi", 2, 128, 14, 14, 128, 3, 3, 1, 1, groups=32), loss_scale=1.0,
+                dy_std=1.0)
+    t1 = base.tensors()
+    a = run_gpu(base, t1)
+    b = run_gpu(base, t1)
+    for k in ("y_bits", "dx_bits", "dw_bits"):
+        assert np.array_equal(a[k], b[k]), k
+    dy1 = I.from_bits(t1["dy"], I.F16)
+    tS = dict(t1)
+    tS["dy"] = I.to_bits(dy1 * 1024.0, I.F16)
     r1 = run_gpu(base, t1, passes=("wgrad",), inv_scale=1.0)
     rS = run_gpu(base, tS, passes=("wgrad",), inv_scale=1.0 / 1024.0)
     assert np.array_equal(r1["dw_bits"], rS["dw_bits"])

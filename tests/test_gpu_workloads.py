@@ -2,8 +2,9 @@
 
 Each seeded workload (the stage-1 bottleneck at batch 64, the stage
 transitions at batch 128, the stem at batch 128, every distinct layer of
-the 53-layer ResNet-50 sweep at batch 256, and the depthwise layers of
-EfficientNet-B0 at batch 128) runs through the same library
+the 53-layer ResNet-50 sweep at batch 256, the depthwise layers of
+EfficientNet-B0 at batch 128 and the grouped layers of ResNeXt-50 at batch
+128) runs through the same library
 calls, descriptors and therefore the same kernel launches that bench.py
 times.  The oracle's single-point routines then evaluate sampled outputs:
 65,536 random positions of y and of dx, every border pixel (all channels) of
@@ -12,7 +13,7 @@ first and last filter in full.  The error is max|err| / max|ref| over the
 sampled positions.  Every output element is also checked for bitwise
 reproducibility across two runs.
 
-Every distinct sweep layer and depthwise layer also runs at batch 3
+Every distinct sweep, depthwise and grouped layer also runs at batch 3
 (ragged tiles) against the full oracle, in fp16 and bf16."""
 import zlib
 
@@ -50,7 +51,7 @@ def workload_cases(cfg, dtype=I.F16):
 
 
 FULL_SIZE = (workload_cases(2) + workload_cases(3) + workload_cases(4) + workload_cases(5) +
-             workload_cases(6))
+             workload_cases(6) + workload_cases(7))
 
 
 def border_and_random(rng, shape, n_random):
@@ -165,6 +166,11 @@ SWEEP_B3 += [("%s %s b3" % (L.name, dt),
                    x_kind="absnormal", dy_std=1e-3, cfg=6, layer_id=li))
              for dt in (I.F16, I.BF16)
              for li, (L, _) in enumerate(I.efficientnet_b0_depthwise(3))]
+SWEEP_B3 += [("%s %s b3" % (L.name, dt),
+              Case(L.with_batch(3), layout="nhwc", dtype=dt, loss_scale=1024.0,
+                   x_kind="absnormal", dy_std=1e-3, cfg=7, layer_id=li))
+             for dt in (I.F16, I.BF16)
+             for li, (L, _) in enumerate(I.resnext50_grouped(3))]
 
 
 @pytest.mark.parametrize("name,case", SWEEP_B3, ids=[c[0] for c in SWEEP_B3])

@@ -41,6 +41,12 @@
  *     aligned activations runs on dedicated vector-ALU kernels (the pass is
  *     bound by memory, not by arithmetic); w and dw are [K][R][S] in both
  *     layouts (one channel per filter).
+ *   - Grouped convolution with m = C/groups = K/groups channels per group,
+ *     m < 64 dividing 64 and c a multiple of 64 (e.g. 32 groups of 4-32
+ *     channels) runs as groups of 64 channels with block-diagonal weights on
+ *     the matrix-core kernels.  Results for finite inputs are those of the
+ *     grouped convolution; a non-finite input value also makes the outputs
+ *     of the other groups sharing its 64-channel block NaN.
  *
  * Errors: every argument check happens on the host before anything is
  * queued.  On a non-OK status nothing is launched and no output or

@@ -76,8 +76,9 @@ bool dw_shape(const Geom &G) {
     return G.n * G.h * G.w * G.c <= lim && G.n * G.p * G.q * G.k <= lim;
 }
 
-// Backward-weight pixel ranges of the depthwise kernel: about 2048
-// workgroups, at least 256 pixels per range.
+// Backward-weight pixel ranges of the gather depthwise kernel: about 2048
+// workgroups, at least 256 pixels per range (the LDS-tiled kernel plans its
+// own splits).
 int32_t dw_wgrad_splits(const Geom &G) {
     const int64_t cblocks = (G.c / 8 + 7) / 8;
     const int64_t npq = G.n * G.p * G.q;
@@ -235,6 +236,8 @@ size_t direct_ws(const Geom &G, nnconv_pass pass) {
     return align256((size_t)plan_wgrad_direct_splits(G) * G.k * G.r * G.s * G.cg * 4);
 }
 
+DWParams dw_params(const Geom &G, float alpha);
+
 // Depthwise workspace: the channel-last copies for NCHW calls, fp32 split
 // partials (backward-weight).
 Regions dw_regions(const Geom &G, nnconv_pass pass) {
@@ -254,7 +257,7 @@ Regions dw_regions(const Geom &G, nnconv_pass pass) {
         if (nchw) { R.a = take(yb); R.c = take(xb); }
     } else {
         if (nchw) { R.a = take(xb); R.b = take(yb); }
-        R.c = take((size_t)dw_wgrad_splits(G) * G.c * G.r * G.s * 4);
+        R.c = take((size_t)dw_params(G, 1.0f).splits * G.c * G.r * G.s * 4);
     }
     R.total = off;
     return R;
@@ -615,7 +618,7 @@ DWParams dw_params(const Geom &G, float alpha) {
     p.cblocks = (int32_t)((G.c / 8 + 7) / 8);
     p.x_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
     p.dy_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
-    p.splits = dw_wgrad_splits(G);
+    p.splits = dw_tiled(p, 2) ? dw_tiled_wgrad_splits(p) : dw_wgrad_splits(G);
     const int64_t npq = G.n * G.p * G.q;
     p.pix_per_split = (npq + p.splits - 1) / p.splits;
     p.alpha = alpha;

@@ -383,6 +383,7 @@ static hipError_t launch_dw_t(int pass, const DWParams &p, const void *a, const 
 
 hipError_t launch_depthwise(int dtype, int pass, const DWParams &p, const void *a, const void *b,
                             void *out, hipStream_t st) {
+    if (dw_tiled(p, pass)) return launch_depthwise_tiled(dtype, pass, p, a, b, out, st);
     if (dtype == Half::id) return launch_dw_t<Half>(pass, p, a, b, out, st);
     return launch_dw_t<BFloat>(pass, p, a, b, out, st);
 }

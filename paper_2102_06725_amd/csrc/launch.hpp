@@ -204,6 +204,26 @@ bool dw_supported(int r, int s);
 hipError_t launch_depthwise(int dtype, int pass, const DWParams &p, const void *a, const void *b,
                             void *out, hipStream_t st);
 
+// LDS-tiled depthwise kernels (depthwise_tiled.hip): equal strides of 1 or 2
+// (backward-data: 1), no dilation.
+struct DWTParams {
+    int32_t n, c, c8, cblocks;
+    int32_t ih, iw, oh, ow;        // input image; output image (forward) or dy
+    int32_t ph, pw;                // top / left padding of the input (may be < 0)
+    int32_t tiles_h, tiles_w;
+    int32_t th;                    // backward-weight: dy rows per tile
+    int32_t tiles_per_split, splits;
+    uint32_t in_bytes, dy_bytes;   // buffer range checks
+    float alpha;
+};
+struct DWWgPlan {
+    int32_t cbv, th, tiles_h, tiles_w, cblocks, splits, tiles_per_split;
+};
+bool dw_tiled(const DWParams &p, int pass);
+int32_t dw_tiled_wgrad_splits(const DWParams &p);
+hipError_t launch_depthwise_tiled(int dtype, int pass, const DWParams &p, const void *a,
+                                  const void *b, void *out, hipStream_t st);
+
 // Training-step pieces (update.hip).  The state type is the C ABI's.
 hipError_t launch_loss_scaler_init(nnconv_loss_scaler *s, float scale, float factor,
                                    int32_t interval, hipStream_t st);

@@ -96,6 +96,26 @@ SMALL = [
     ("depthwise 5x5 stride 3 ragged", Case(L("dw7", 3, 8, 11, 13, 8, 5, 5, 3, 1, groups=8))),
     ("depthwise 3x3 H = W = 1", Case(L("dw8", 4, 32, 1, 1, 32, 3, 3, 1, 1, groups=32))),
     ("direct: depthwise C12", Case(L("dw9", 2, 12, 9, 9, 12, 3, 3, 1, 1, groups=12))),
+    # LDS-tiled depthwise: channel blocks of 2 / 4 / 8 vectors, ragged tiles,
+    # padding above R-1 (negative padding of the rotated backward-data),
+    # 7x7 weights in LDS, several tiles per backward-weight split
+    ("depthwise tiled C16 ragged", Case(L("dt1", 2, 16, 37, 35, 16, 3, 3, 1, 1, groups=16))),
+    ("depthwise tiled C48 stride 2 odd width", Case(L("dt2", 3, 48, 23, 29, 48, 3, 3, 2, 1,
+                                                      groups=48))),
+    ("depthwise tiled 5x5 C144", Case(L("dt3", 2, 144, 19, 21, 144, 5, 5, 1, 2, groups=144))),
+    ("depthwise tiled 7x7 C72 stride 2", Case(L("dt4", 2, 72, 25, 22, 72, 7, 7, 2, 3,
+                                                groups=72))),
+    ("depthwise tiled 7x7 C64", Case(L("dt5", 2, 64, 17, 18, 64, 7, 7, 1, 3, groups=64))),
+    ("depthwise tiled 3x3 pad 2", Case(L("dt6", 2, 32, 10, 12, 32, 3, 3, 1, 2, groups=32))),
+    ("depthwise tiled 3x3 pad 3 C24", Case(L("dt7", 1, 24, 6, 7, 24, 3, 3, 1, 3, groups=24))),
+    ("depthwise tiled 5x5 stride 2 pad 0", Case(L("dt8", 6, 40, 33, 30, 40, 5, 5, 2, 0,
+                                                  groups=40))),
+    ("depthwise tiled 5x5 bf16", Case(L("dt9", 2, 96, 15, 17, 96, 5, 5, 1, 2, groups=96),
+                                      dtype=I.BF16)),
+    ("depthwise tiled many tiles per split", Case(L("dt10", 40, 8, 64, 64, 8, 3, 3, 1, 1,
+                                                    groups=8))),
+    ("depthwise tiled 3x3 stride 2 NCHW bf16", Case(L("dt11", 2, 56, 13, 16, 56, 3, 3, 2, 1,
+                                                      groups=56), layout="nchw", dtype=I.BF16)),
     # small groups (Cg = Kg < 64) as 64-channel super-groups
     ("groups 32 x 4 channels", Case(L("sg4", 2, 128, 9, 10, 128, 3, 3, 1, 1, groups=32))),
     ("groups 32 x 8 channels stride 2", Case(L("sg8", 2, 256, 9, 8, 256, 3, 3, 2, 1,

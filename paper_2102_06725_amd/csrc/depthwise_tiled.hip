@@ -12,6 +12,9 @@
 //     (vector, column, row group) computes TP output rows of one column and
 //     reads each input row of its strip once; the weights of its 8 channels
 //     stay in registers (LDS for 7x7);
+//   - backward-data at stride 2: a workgroup owns a tile of dx and the dy
+//     pixels it reaches; each output adds only the taps of its row and
+//     column parity;
 //   - backward-weight: a workgroup owns one channel block and a run of
 //     spatial tiles of dy; thread (vector, filter row r, dy row) adds the S
 //     taps of filter row r over its dy row with a sliding window of input
@@ -102,6 +105,23 @@ struct FwdTile {
     static constexpr int CHUNKS = IH * IW * CBV;  // 16-byte vectors
     static constexpr int NL = (CHUNKS + 255) / 256;
     static constexpr bool WREG = R <= 5;
+};
+
+// Stride-2 backward-data tile: TH x TW dx pixels, laid out over the threads
+// like the stride-1 forward tile; dy tile DH x DW pixels.  Each output takes
+// the taps of its row and column parity: ceil(R/2) or floor(R/2) filter rows
+// and columns.
+template <int R, int CBV>
+struct Dg2Tile {
+    static constexpr int TP = R <= 5 ? 4 : 2;  // even: a strip starts on an even row
+    static constexpr int TW = CBV == 2 ? 32 : 16;
+    static constexpr int RG = 256 / (CBV * TW);
+    static constexpr int TH = RG * TP;
+    static constexpr int DH = (TH + R + 1) / 2;
+    static constexpr int DW = (TW + R + 1) / 2;
+    static constexpr int CHUNKS = DH * DW * CBV;
+    static constexpr int NL = (CHUNKS + 255) / 256;
+    static constexpr int KS = (R + 1) / 2;  // column taps of one parity (the last may be absent)
 };
 
 // Backward-weight tile: dy rows (at most GMAX, one per thread row group) x
@@ -234,6 +254,107 @@ __global__ __launch_bounds__(256) void dwt_fwd_kernel(const DWTParams P,
         for (int i = 0; i < F::TP; ++i) {
             const int oh = oh0 + rg * F::TP + i;
             if (oh < P.oh) *(u32x4 *)(o + (int64_t)oh * P.ow * P.c) = pack8<T>(acc[i], P.alpha);
+        }
+    }
+}
+
+// Stride 2: dx[n, i, j, c] = alpha * sum over the taps (r, s) with i + ph - r
+// and j + pw - s even of dy[n, (i+ph-r)/2, (j+pw-s)/2, c] * w[c, r, s].
+// PHP = ph % 2 fixes, for each strip row, which filter rows reach it; the
+// column parity varies by lane and selects the lane's weight columns once.
+template <class T, int R, int CBV, int PHP>
+__global__ __launch_bounds__(256) void dwt_dgrad2_kernel(const DWTParams P,
+                                                         const uint16_t *__restrict__ dy,
+                                                         const uint16_t *__restrict__ w,
+                                                         uint16_t *__restrict__ dx) {
+    using namespace dwt;
+    using G = Dg2Tile<R, CBV>;
+    constexpr int S = R, RS = R * S, CW = CBV * 8, KS = G::KS;
+    __shared__ u32x4 tile[G::CHUNKS];
+    __shared__ __attribute__((aligned(16))) uint16_t wl[R * (S + 1)][CW];  // column S: zeros
+    const int tid = threadIdx.x;
+
+    uint32_t b = xcd_remap(blockIdx.x, gridDim.x);
+    const int cb = (int)(b % (uint32_t)P.cblocks);
+    b /= (uint32_t)P.cblocks;
+    const int tw = (int)(b % (uint32_t)P.tiles_w);
+    b /= (uint32_t)P.tiles_w;
+    const int th = (int)(b % (uint32_t)P.tiles_h);
+    const int n = (int)(b / (uint32_t)P.tiles_h);
+    const int i0 = th * G::TH, j0 = tw * G::TW;  // both even
+    // first dy row / column any output of the tile reaches (floor division)
+    const int p0 = (i0 + P.ph - (R - 1)) >> 1;
+    const int q0 = (j0 + P.pw - (S - 1)) >> 1;
+
+    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(dy, P.in_bytes);
+    const uint32_t img = (uint32_t)n * (uint32_t)P.ih;
+    u32x4 ld[G::NL];
+#pragma unroll
+    for (int k = 0; k < G::NL; ++k) {
+        const int e = k * 256 + tid;
+        const int row = e / (G::DW * CBV);
+        const int rem = e - row * (G::DW * CBV);
+        const int col = rem / CBV, cvl = rem - col * CBV;
+        const int p = p0 + row, q = q0 + col, cvec = cb * CBV + cvl;
+        const bool ok = e < G::CHUNKS && (unsigned)p < (unsigned)P.ih && (unsigned)q < (unsigned)P.iw &&
+                        cvec < P.c8;
+        const uint32_t off = ((img + (uint32_t)p) * (uint32_t)P.iw + (uint32_t)q) * (uint32_t)P.c * 2u +
+                             (uint32_t)cvec * 16u;
+        ld[k] = load16(rdy, ok ? off : OOB_OFFSET);
+    }
+    for (int e = tid; e < R * (S + 1) * CW; e += 256) {
+        const int cl = e / (R * (S + 1)), t = e - cl * (R * (S + 1));
+        const int r = t / (S + 1), sc = t - r * (S + 1);
+        const int ch = cb * CW + cl;
+        wl[t][cl] = (sc < S && ch < P.c) ? w[(int64_t)ch * RS + r * S + sc] : (uint16_t)0;
+    }
+#pragma unroll
+    for (int k = 0; k < G::NL; ++k) {
+        const int e = k * 256 + tid;
+        if (G::NL * 256 == G::CHUNKS || e < G::CHUNKS) tile[e] = ld[k];
+    }
+    __syncthreads();
+
+    const int cv = tid % CBV;
+    const int col = (tid / CBV) % G::TW;
+    const int rg = tid / (CBV * G::TW);
+    // columns s = s0, s0 + 2, ... reach this lane's output column
+    const int s0 = (col + P.pw) & 1;
+    u32x4 wr[R][KS];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int k = 0; k < KS; ++k) wr[r][k] = *(const u32x4 *)&wl[r * (S + 1) + s0 + 2 * k][cv * 8];
+    // dy tile column of tap s0 + 2k: qb - k
+    const int qb = ((P.pw & 1) + col + S - 1 - s0) >> 1;
+    float acc[G::TP][8];
+#pragma unroll
+    for (int t = 0; t < G::TP; ++t)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[t][k] = 0.f;
+#pragma unroll
+    for (int t = 0; t < G::TP; ++t) {
+#pragma unroll
+        for (int r = (t + PHP) & 1; r < R; r += 2) {
+            // dy tile row of output row i0 + rg*TP + t through filter row r
+            const int prow = rg * (G::TP / 2) + (PHP + t + R - 1 - r) / 2;
+            const u32x4 *trow = tile + (prow * G::DW + qb) * CBV + cv;
+#pragma unroll
+            for (int k = 0; k < KS; ++k) {
+                if (S % 2 == 1 && k == KS - 1 && s0 == 1) continue;  // tap s0 + 2k == S
+                fma8<T, true>(acc[t], trow[-k * CBV], wr[r][k]);
+            }
+        }
+    }
+
+    const int cvec = cb * CBV + cv;
+    const int j = j0 + col;
+    if (cvec < P.c8 && j < P.ow) {
+        uint16_t *o = dx + ((int64_t)n * P.oh * P.ow + j) * P.c + cvec * 8;
+#pragma unroll
+        for (int t = 0; t < G::TP; ++t) {
+            const int i = i0 + rg * G::TP + t;
+            if (i < P.oh) *(u32x4 *)(o + (int64_t)i * P.ow * P.c) = pack8<T>(acc[t], P.alpha);
         }
     }
 }
@@ -443,6 +564,41 @@ hipError_t launch_fwd_t(const DWTParams &q, int r, int sh, const void *in, const
     return hipErrorInvalidValue;
 }
 
+template <class T, int R, int CBV, int PHP>
+hipError_t launch_dgrad2_cfg(DWTParams q, const void *dy, const void *w, void *dx, hipStream_t st) {
+    using G = dwt::Dg2Tile<R, CBV>;
+    q.cblocks = (q.c8 + CBV - 1) / CBV;
+    q.tiles_h = (q.oh + G::TH - 1) / G::TH;
+    q.tiles_w = (q.ow + G::TW - 1) / G::TW;
+    const int64_t nb = (int64_t)q.n * q.tiles_h * q.tiles_w * q.cblocks;
+    if (nb <= 0) return hipSuccess;
+    if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((dwt_dgrad2_kernel<T, R, CBV, PHP>), dim3((uint32_t)nb), dim3(256), 0, st, q,
+                       (const uint16_t *)dy, (const uint16_t *)w, (uint16_t *)dx);
+    return hipGetLastError();
+}
+
+template <class T, int R, int PHP>
+hipError_t launch_dgrad2_rs(const DWTParams &q, const void *dy, const void *w, void *dx, hipStream_t st) {
+    // the stride-2 backward-data tile has the stride-1 forward tile's shape
+    switch (pick_fwd_cbv(q, R, 1)) {
+        case 2: return launch_dgrad2_cfg<T, R, 2, PHP>(q, dy, w, dx, st);
+        case 4: return launch_dgrad2_cfg<T, R, 4, PHP>(q, dy, w, dx, st);
+        default: return launch_dgrad2_cfg<T, R, 8, PHP>(q, dy, w, dx, st);
+    }
+}
+
+template <class T, int PHP>
+hipError_t launch_dgrad2_t(const DWTParams &q, int r, const void *dy, const void *w, void *dx,
+                           hipStream_t st) {
+    switch (r) {
+        case 3: return launch_dgrad2_rs<T, 3, PHP>(q, dy, w, dx, st);
+        case 5: return launch_dgrad2_rs<T, 5, PHP>(q, dy, w, dx, st);
+        case 7: return launch_dgrad2_rs<T, 7, PHP>(q, dy, w, dx, st);
+    }
+    return hipErrorInvalidValue;
+}
+
 int wg_gmax(int r, int cbv) { return 256 / (cbv * r); }
 
 // Backward-weight tiling: per CBV, dy rows per tile balanced over the image
@@ -540,7 +696,7 @@ bool dw_tiled(const DWParams &p, int pass) {
     const bool plain = p.r == p.s && p.sh == p.sw && p.dh == 1 && p.dw == 1 &&
                        (p.r == 3 || p.r == 5 || p.r == 7);
     if (!plain) return false;
-    return pass == 1 ? p.sh == 1 : (p.sh == 1 || p.sh == 2);
+    return p.sh == 1 || p.sh == 2;
 }
 
 int32_t dw_tiled_wgrad_splits(const DWParams &p) { return plan_wgrad(p).splits; }
@@ -563,10 +719,18 @@ hipError_t launch_depthwise_tiled(int dtype, int pass, const DWParams &p, const 
         if (dtype == Half::id) return launch_fwd_t<Half, false>(q, p.r, p.sh, a, b, out, st);
         return launch_fwd_t<BFloat, false>(q, p.r, p.sh, a, b, out, st);
     }
-    // stride 1 backward-data: dy -> dx with the rotated filter
     q.ih = p.p; q.iw = p.q; q.oh = p.h; q.ow = p.w;
-    q.ph = p.r - 1 - p.ph; q.pw = p.s - 1 - p.pw;
     q.in_bytes = p.dy_bytes;
+    if (p.sh == 2) {  // dy -> dx, taps by output parity
+        q.ph = p.ph; q.pw = p.pw;
+        if (dtype == Half::id)
+            return (p.ph & 1) ? launch_dgrad2_t<Half, 1>(q, p.r, a, b, out, st)
+                              : launch_dgrad2_t<Half, 0>(q, p.r, a, b, out, st);
+        return (p.ph & 1) ? launch_dgrad2_t<BFloat, 1>(q, p.r, a, b, out, st)
+                          : launch_dgrad2_t<BFloat, 0>(q, p.r, a, b, out, st);
+    }
+    // stride 1: dy -> dx with the rotated filter
+    q.ph = p.r - 1 - p.ph; q.pw = p.s - 1 - p.pw;
     if (dtype == Half::id) return launch_fwd_t<Half, true>(q, p.r, 1, a, b, out, st);
     return launch_fwd_t<BFloat, true>(q, p.r, 1, a, b, out, st);
 }

@@ -204,8 +204,8 @@ bool dw_supported(int r, int s);
 hipError_t launch_depthwise(int dtype, int pass, const DWParams &p, const void *a, const void *b,
                             void *out, hipStream_t st);
 
-// LDS-tiled depthwise kernels (depthwise_tiled.hip): equal strides of 1 or 2
-// (backward-data: 1), no dilation.
+// LDS-tiled depthwise kernels (depthwise_tiled.hip): equal strides of 1 or 2,
+// no dilation.
 struct DWTParams {
     int32_t n, c, c8, cblocks;
     int32_t ih, iw, oh, ow;        // input image; output image (forward) or dy

@@ -114,6 +114,12 @@ SMALL = [
                                       dtype=I.BF16)),
     ("depthwise tiled many tiles per split", Case(L("dt10", 40, 8, 64, 64, 8, 3, 3, 1, 1,
                                                     groups=8))),
+    ("depthwise tiled 3x3 stride 2 pad 0", Case(L("dt12", 2, 32, 17, 18, 32, 3, 3, 2, 0,
+                                                  groups=32))),
+    ("depthwise tiled 5x5 stride 2 pad 1 C16", Case(L("dt13", 3, 16, 21, 19, 16, 5, 5, 2, 1,
+                                                      groups=16))),
+    ("depthwise tiled 3x3 stride 2 pad 2 even size", Case(L("dt14", 2, 64, 16, 14, 64, 3, 3, 2,
+                                                            2, groups=64))),
     ("depthwise tiled 3x3 stride 2 NCHW bf16", Case(L("dt11", 2, 56, 13, 16, 56, 3, 3, 2, 1,
                                                       groups=56), layout="nchw", dtype=I.BF16)),
     # small groups (Cg = Kg < 64) as 64-channel super-groups

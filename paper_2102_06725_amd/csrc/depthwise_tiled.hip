@@ -373,8 +373,12 @@ __global__ __launch_bounds__(256) void dwt_wgrad_kernel(const DWTParams P,
     __shared__ u32x4 dt[W::DCH];
     __shared__ float red[256 * 8];
     const int tid = threadIdx.x;
-    const int cb = (int)blockIdx.x;
-    const int split = (int)blockIdx.y;
+    // the channel blocks of one split run back to back on one XCD: a block
+    // of fewer than 8 vectors uses only part of each 128-byte line, and the
+    // other blocks' workgroups then find the rest in the same L2
+    const uint32_t b = xcd_remap(blockIdx.x, gridDim.x);
+    const int cb = (int)(b % (uint32_t)P.cblocks);
+    const int split = (int)(b / (uint32_t)P.cblocks);
     const int ntiles = P.n * P.tiles_h * P.tiles_w;
     const int t_begin = split * P.tiles_per_split;
     const int t_end = min(ntiles, t_begin + P.tiles_per_split);
@@ -656,8 +660,10 @@ hipError_t launch_wgrad_cfg(const DWParams &p, const DWWgPlan &pl, const void *x
     q.in_bytes = p.x_bytes; q.dy_bytes = p.dy_bytes;
     q.alpha = 1.f;
     if (pl.th > dwt::WgTile<R, SH, CBV>::GMAX || pl.splits != p.splits) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((dwt_wgrad_kernel<T, R, SH, CBV>), dim3((uint32_t)pl.cblocks, (uint32_t)pl.splits),
-                       dim3(256), 0, st, q, (const uint16_t *)x, (const uint16_t *)dy, ws);
+    const int64_t nb = (int64_t)pl.cblocks * pl.splits;
+    if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((dwt_wgrad_kernel<T, R, SH, CBV>), dim3((uint32_t)nb), dim3(256), 0, st, q,
+                       (const uint16_t *)x, (const uint16_t *)dy, ws);
     return hipGetLastError();
 }
 

@@ -92,11 +92,15 @@ __device__ __forceinline__ int tapcol(int col, int s) {
 }
 
 // Forward tile: 256 threads = CBV vectors x TW columns x RG row groups of TP
-// rows.  Input tile IH x IW pixels.
-template <int R, int SH, int CBV>
+// rows.  Input tile IH x IW pixels.  The narrow tile (stride 1) has half the
+// columns and half the rows per thread, for images narrower than the wide
+// tile (7x7).
+template <int R, int SH, int CBV, bool NARROW>
 struct FwdTile {
-    static constexpr int TP = (SH == 1 && R <= 5) ? 4 : 2;
-    static constexpr int TW = SH == 1 ? (CBV == 2 ? 32 : 16) : 64 / CBV;
+    static constexpr int TPW = (SH == 1 && R <= 5) ? 4 : 2;
+    static constexpr int TWW = SH == 1 ? (CBV == 2 ? 32 : 16) : 64 / CBV;
+    static constexpr int TP = NARROW ? (TPW > 1 ? TPW / 2 : 1) : TPW;
+    static constexpr int TW = NARROW ? TWW / 2 : TWW;
     static constexpr int RG = 256 / (CBV * TW);
     static constexpr int TH = RG * TP;
     static constexpr int IH = (TH - 1) * SH + R;
@@ -111,10 +115,10 @@ struct FwdTile {
 // like the stride-1 forward tile; dy tile DH x DW pixels.  Each output takes
 // the taps of its row and column parity: ceil(R/2) or floor(R/2) filter rows
 // and columns.
-template <int R, int CBV>
+template <int R, int CBV, bool NARROW>
 struct Dg2Tile {
-    static constexpr int TP = R <= 5 ? 4 : 2;  // even: a strip starts on an even row
-    static constexpr int TW = CBV == 2 ? 32 : 16;
+    static constexpr int TP = (R <= 5 && !NARROW) ? 4 : 2;  // even: a strip starts on an even row
+    static constexpr int TW = (CBV == 2 ? 32 : 16) / (NARROW ? 2 : 1);
     static constexpr int RG = 256 / (CBV * TW);
     static constexpr int TH = RG * TP;
     static constexpr int DH = (TH + R + 1) / 2;
@@ -146,13 +150,13 @@ struct WgTile {
 
 // out[n, o, u, c] = alpha * sum_{r,s} in[n, o*SH - ph + r, u*SH - pw + s, c] * w'[c, r, s]
 // with w' = w, or w rotated by 180 degrees (FLIP).
-template <class T, int R, int SH, int CBV, bool FLIP>
+template <class T, int R, int SH, int CBV, bool NARROW, bool FLIP>
 __global__ __launch_bounds__(256) void dwt_fwd_kernel(const DWTParams P,
                                                       const uint16_t *__restrict__ in,
                                                       const uint16_t *__restrict__ w,
                                                       uint16_t *__restrict__ out) {
     using namespace dwt;
-    using F = FwdTile<R, SH, CBV>;
+    using F = FwdTile<R, SH, CBV, NARROW>;
     constexpr int S = R, RS = R * S, CW = CBV * 8;
     __shared__ u32x4 tile[F::CHUNKS];
     __shared__ __attribute__((aligned(16))) uint16_t wl[RS][CW];
@@ -262,13 +266,13 @@ __global__ __launch_bounds__(256) void dwt_fwd_kernel(const DWTParams P,
 // and j + pw - s even of dy[n, (i+ph-r)/2, (j+pw-s)/2, c] * w[c, r, s].
 // PHP = ph % 2 fixes, for each strip row, which filter rows reach it; the
 // column parity varies by lane and selects the lane's weight columns once.
-template <class T, int R, int CBV, int PHP>
+template <class T, int R, int CBV, bool NARROW, int PHP>
 __global__ __launch_bounds__(256) void dwt_dgrad2_kernel(const DWTParams P,
                                                          const uint16_t *__restrict__ dy,
                                                          const uint16_t *__restrict__ w,
                                                          uint16_t *__restrict__ dx) {
     using namespace dwt;
-    using G = Dg2Tile<R, CBV>;
+    using G = Dg2Tile<R, CBV, NARROW>;
     constexpr int S = R, RS = R * S, CW = CBV * 8, KS = G::KS;
     __shared__ u32x4 tile[G::CHUNKS];
     __shared__ __attribute__((aligned(16))) uint16_t wl[R * (S + 1)][CW];  // column S: zeros
@@ -501,51 +505,79 @@ namespace {
 
 constexpr int CBV_CHOICES[3] = {8, 4, 2};
 
-// forward tile sizes by CBV (FwdTile's TH / TW without instantiating it)
-void fwd_tile_dims(int r, int sh, int cbv, int *th, int *tw) {
-    const int tp = (sh == 1 && r <= 5) ? 4 : 2;
-    *tw = sh == 1 ? (cbv == 2 ? 32 : 16) : 64 / cbv;
-    *th = 256 / (cbv * *tw) * tp;
+// tile sizes (rows, columns, rows per thread) without instantiating the
+// kernels: kind 0 = forward / stride-1 backward-data, 1 = stride-2
+// backward-data
+void tile_dims(int kind, int r, int sh, int cbv, bool narrow, int *th, int *tw, int *tp) {
+    if (kind == 0) {
+        const int tpw = (sh == 1 && r <= 5) ? 4 : 2;
+        const int tww = sh == 1 ? (cbv == 2 ? 32 : 16) : 64 / cbv;
+        *tp = narrow ? (tpw > 1 ? tpw / 2 : 1) : tpw;
+        *tw = narrow ? tww / 2 : tww;
+    } else {
+        *tp = (r <= 5 && !narrow) ? 4 : 2;
+        *tw = (cbv == 2 ? 32 : 16) / (narrow ? 2 : 1);
+    }
+    *th = 256 / (cbv * *tw) * *tp;
 }
 
-// the CBV whose launch has the fewest workgroups (every workgroup does the
-// same work: 256 threads x TP outputs); ties go to the wider block
-int pick_fwd_cbv(const DWTParams &q, int r, int sh) {
-    int best = 8;
+// The (CBV, narrow) pair with the least work: workgroups x rows per thread
+// (every thread of a workgroup computes its rows, inside the image or not);
+// ties go to the wide tile and the wider block.  Narrow tiles only at
+// stride 1 (kind 0) or for backward-data.
+struct TilePick {
+    int cbv;
+    bool narrow;
+};
+TilePick pick_tile(const DWTParams &q, int kind, int r, int sh) {
+    TilePick best = {8, false};
     int64_t best_cost = -1;
-    for (int cbv : CBV_CHOICES) {
-        int th, tw;
-        fwd_tile_dims(r, sh, cbv, &th, &tw);
-        const int64_t cost = (int64_t)((q.c8 + cbv - 1) / cbv) * ((q.oh + th - 1) / th) *
-                             ((q.ow + tw - 1) / tw);
-        if (best_cost < 0 || cost < best_cost) {
-            best = cbv;
-            best_cost = cost;
+    for (int nw = 0; nw < 2; ++nw) {
+        if (nw && kind == 0 && sh != 1) continue;
+        for (int cbv : CBV_CHOICES) {
+            int th, tw, tp;
+            tile_dims(kind, r, sh, cbv, nw != 0, &th, &tw, &tp);
+            const int64_t cost = (int64_t)((q.c8 + cbv - 1) / cbv) * ((q.oh + th - 1) / th) *
+                                 ((q.ow + tw - 1) / tw) * tp;
+            if (best_cost < 0 || cost < best_cost) {
+                best = {cbv, nw != 0};
+                best_cost = cost;
+            }
         }
     }
     return best;
 }
 
-template <class T, int R, int SH, int CBV, bool FLIP>
+template <class T, int R, int SH, int CBV, bool NARROW, bool FLIP>
 hipError_t launch_fwd_cfg(DWTParams q, const void *in, const void *w, void *out, hipStream_t st) {
-    using F = dwt::FwdTile<R, SH, CBV>;
+    using F = dwt::FwdTile<R, SH, CBV, NARROW>;
     q.cblocks = (q.c8 + CBV - 1) / CBV;
     q.tiles_h = (q.oh + F::TH - 1) / F::TH;
     q.tiles_w = (q.ow + F::TW - 1) / F::TW;
     const int64_t nb = (int64_t)q.n * q.tiles_h * q.tiles_w * q.cblocks;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((dwt_fwd_kernel<T, R, SH, CBV, FLIP>), dim3((uint32_t)nb), dim3(256), 0, st, q,
-                       (const uint16_t *)in, (const uint16_t *)w, (uint16_t *)out);
+    hipLaunchKernelGGL((dwt_fwd_kernel<T, R, SH, CBV, NARROW, FLIP>), dim3((uint32_t)nb), dim3(256), 0,
+                       st, q, (const uint16_t *)in, (const uint16_t *)w, (uint16_t *)out);
     return hipGetLastError();
 }
 
 template <class T, int R, int SH, bool FLIP>
 hipError_t launch_fwd_rs(const DWTParams &q, const void *in, const void *w, void *out, hipStream_t st) {
-    switch (pick_fwd_cbv(q, R, SH)) {
-        case 2: return launch_fwd_cfg<T, R, SH, 2, FLIP>(q, in, w, out, st);
-        case 4: return launch_fwd_cfg<T, R, SH, 4, FLIP>(q, in, w, out, st);
-        default: return launch_fwd_cfg<T, R, SH, 8, FLIP>(q, in, w, out, st);
+    const TilePick t = pick_tile(q, 0, R, SH);
+    if constexpr (SH == 1) {
+        if (t.narrow) {
+            switch (t.cbv) {
+                case 2: return launch_fwd_cfg<T, R, SH, 2, true, FLIP>(q, in, w, out, st);
+                case 4: return launch_fwd_cfg<T, R, SH, 4, true, FLIP>(q, in, w, out, st);
+                default: return launch_fwd_cfg<T, R, SH, 8, true, FLIP>(q, in, w, out, st);
+            }
+        }
+    }
+    switch (t.cbv) {
+        case 2: return launch_fwd_cfg<T, R, SH, 2, false, FLIP>(q, in, w, out, st);
+        case 4: return launch_fwd_cfg<T, R, SH, 4, false, FLIP>(q, in, w, out, st);
+        default: return launch_fwd_cfg<T, R, SH, 8, false, FLIP>(q, in, w, out, st);
     }
 }
 
@@ -568,27 +600,34 @@ hipError_t launch_fwd_t(const DWTParams &q, int r, int sh, const void *in, const
     return hipErrorInvalidValue;
 }
 
-template <class T, int R, int CBV, int PHP>
+template <class T, int R, int CBV, bool NARROW, int PHP>
 hipError_t launch_dgrad2_cfg(DWTParams q, const void *dy, const void *w, void *dx, hipStream_t st) {
-    using G = dwt::Dg2Tile<R, CBV>;
+    using G = dwt::Dg2Tile<R, CBV, NARROW>;
     q.cblocks = (q.c8 + CBV - 1) / CBV;
     q.tiles_h = (q.oh + G::TH - 1) / G::TH;
     q.tiles_w = (q.ow + G::TW - 1) / G::TW;
     const int64_t nb = (int64_t)q.n * q.tiles_h * q.tiles_w * q.cblocks;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((dwt_dgrad2_kernel<T, R, CBV, PHP>), dim3((uint32_t)nb), dim3(256), 0, st, q,
-                       (const uint16_t *)dy, (const uint16_t *)w, (uint16_t *)dx);
+    hipLaunchKernelGGL((dwt_dgrad2_kernel<T, R, CBV, NARROW, PHP>), dim3((uint32_t)nb), dim3(256), 0, st,
+                       q, (const uint16_t *)dy, (const uint16_t *)w, (uint16_t *)dx);
     return hipGetLastError();
 }
 
 template <class T, int R, int PHP>
 hipError_t launch_dgrad2_rs(const DWTParams &q, const void *dy, const void *w, void *dx, hipStream_t st) {
-    // the stride-2 backward-data tile has the stride-1 forward tile's shape
-    switch (pick_fwd_cbv(q, R, 1)) {
-        case 2: return launch_dgrad2_cfg<T, R, 2, PHP>(q, dy, w, dx, st);
-        case 4: return launch_dgrad2_cfg<T, R, 4, PHP>(q, dy, w, dx, st);
-        default: return launch_dgrad2_cfg<T, R, 8, PHP>(q, dy, w, dx, st);
+    const TilePick t = pick_tile(q, 1, R, 2);
+    if (t.narrow) {
+        switch (t.cbv) {
+            case 2: return launch_dgrad2_cfg<T, R, 2, true, PHP>(q, dy, w, dx, st);
+            case 4: return launch_dgrad2_cfg<T, R, 4, true, PHP>(q, dy, w, dx, st);
+            default: return launch_dgrad2_cfg<T, R, 8, true, PHP>(q, dy, w, dx, st);
+        }
+    }
+    switch (t.cbv) {
+        case 2: return launch_dgrad2_cfg<T, R, 2, false, PHP>(q, dy, w, dx, st);
+        case 4: return launch_dgrad2_cfg<T, R, 4, false, PHP>(q, dy, w, dx, st);
+        default: return launch_dgrad2_cfg<T, R, 8, false, PHP>(q, dy, w, dx, st);
     }
 }
 

@@ -120,6 +120,10 @@ SMALL = [
                                                       groups=16))),
     ("depthwise tiled 3x3 stride 2 pad 2 even size", Case(L("dt14", 2, 64, 16, 14, 64, 3, 3, 2,
                                                             2, groups=64))),
+    ("depthwise tiled 5x5 on 7x7 (narrow tile)", Case(L("dt15", 3, 128, 7, 7, 128, 5, 5, 1, 2,
+                                                        groups=128))),
+    ("depthwise tiled stride 2 on 7x7 (narrow)", Case(L("dt16", 2, 64, 7, 7, 64, 3, 3, 2, 1,
+                                                        groups=64))),
     ("depthwise tiled 3x3 stride 2 NCHW bf16", Case(L("dt11", 2, 56, 13, 16, 56, 3, 3, 2, 1,
                                                       groups=56), layout="nchw", dtype=I.BF16)),
     # small groups (Cg = Kg < 64) as 64-channel super-groups

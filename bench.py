@@ -214,7 +214,8 @@ def is_forward_launch(names, i):
     depthwise-forward dispatch that follows a non-library dispatch, a split
     reduction or a padding copy."""
     n = names[i]
-    if "nnconv::" not in n or not ("igemm" in n or "stem_fwd" in n or "dw_fwd" in n):
+    if "nnconv::" not in n or not ("igemm" in n or "stem_fwd" in n or "dw_fwd" in n or
+                                   "dwt_fwd" in n):
         return False
     if i == 0:
         return True
@@ -502,7 +503,8 @@ def main():
         if depthwise:
             fwd_bytes = sum(compulsory_bytes(L, "fwd") for L in layers) / len(layers)
             gbs = fwd_bytes / (fwd_avg_ms * 1e-3) / 1e9
-            roofline = {"kernel": "dw_fwd_kernel, one launch per nnconv_fwd call",
+            roofline = {"kernel": "depthwise forward (dwt_fwd_kernel), one launch per "
+                                  "nnconv_fwd call",
                         "bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": gbs / PEAK_HBM_GBS, "traffic": None,
                         "avg_launch_us": fwd_avg_ms * 1e3,

@@ -38,9 +38,9 @@
  *   - Depthwise convolution (groups == c == k, one channel per group, the
  *     MobileNet / EfficientNet layers trained with the paper's framework)
  *     with c a multiple of 8, a square 3x3, 5x5 or 7x7 filter and 16-byte
- *     aligned activations runs on dedicated vector-ALU kernels (the pass is
- *     bound by memory, not by arithmetic); w and dw are [K][R][S] in both
- *     layouts (one channel per filter).
+ *     aligned activations runs on dedicated vector-ALU kernels (R*S
+ *     multiply-adds per output are too few for the matrix cores); w and dw
+ *     are [K][R][S] in both layouts (one channel per filter).
  *   - Grouped convolution with m = C/groups = K/groups channels per group,
  *     m < 64 dividing 64 and c a multiple of 64 (e.g. 32 groups of 4-32
  *     channels) runs as groups of 64 channels with block-diagonal weights on

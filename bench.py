@@ -13,7 +13,9 @@ inputs are seeded synthetic draws already resident in HBM.  Prints one
 JSON line.
 
 value = sum of algorithmic FLOPs (2*N*K*P*Q*Cg*R*S per pass, stem with its
-3 logical channels) / wall time of the timed steps.
+3 logical channels) / wall time of the timed steps.  The timed steps carry
+no markers; per-pass times and the forward launch durations come from the
+same number of steps run again afterwards with HIP events around every pass.
 """
 from __future__ import annotations
 
@@ -53,7 +55,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=30.0,
                     help="upper bound on the oracle CPU-baseline sample (0 disables it)")
     ap.add_argument("--no-events", action="store_true",
-                    help="skip the per-call HIP events inside the timed steps")
+                    help="skip the event-instrumented steps (per-pass times, roofline)")
     ap.add_argument("--layers", default="",
                     help="comma-separated layer names: run only these layers of the workload "
                          "(for profiling one shape; the reported value then covers only them)")
@@ -282,10 +284,14 @@ def summarize_profile(args):
     print("\n".join(out))
 
 
+CPU_SAMPLE_BATCH = 16  # about 10-15 s of oracle work for the ResNet-50 shapes
+
+
 def cpu_baseline(args, wl):
     """The fp64 oracle as it stands, timed on this host's cores over a bounded
-    sample: every distinct layer shape of the workload at batch 8, all its
-    passes, stopping once the time bound is reached."""
+    sample: every distinct layer shape of the workload at batch
+    CPU_SAMPLE_BATCH, all its passes, stopping once the time bound is
+    reached."""
     import numpy as np
     import oracle.oracle as orc
     from paper_2102_06725_amd import inputs as I
@@ -301,7 +307,7 @@ def cpu_baseline(args, wl):
     done = 0
     passes_done = 0
     for li, L in enumerate(seen):
-        Ls = L.with_batch(8)
+        Ls = L.with_batch(CPU_SAMPLE_BATCH)
         cl = Ls.c_alg
         cv = orc.Conv(Ls.n, cl, Ls.h, Ls.w, Ls.k, Ls.r, Ls.s, (Ls.stride,) * 2, (Ls.pad,) * 2,
                       (Ls.dil,) * 2, Ls.groups)
@@ -328,9 +334,9 @@ def cpu_baseline(args, wl):
         "unit": "TFLOP/s",
         "cores": orc.get_threads(),
         "kind": "oracle",
-        "sample": "fp64 direct-loop oracle, %d of %d distinct layer shapes at batch 8 "
-                  "(%d passes, %.1f GFLOP) in %.1f s" % (done, len(seen), passes_done,
-                                                        flops / 1e9, t_total),
+        "sample": "fp64 direct-loop oracle, %d of %d distinct layer shapes at batch %d "
+                  "(%d passes, %.1f GFLOP) in %.1f s" % (done, len(seen), CPU_SAMPLE_BATCH,
+                                                        passes_done, flops / 1e9, t_total),
     }
 
 
@@ -438,20 +444,28 @@ def main():
         one_step(None)
     torch.cuda.synchronize()
 
-    use_ev = not args.no_events
-    ev_steps = []
+    # The timed steps carry no markers: an event record between every two
+    # launches costs about 0.7 ms per step of the ResNet-50 sweep.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in bufs] if use_ev else None
-        one_step(ev)
-        if use_ev:
-            ev_steps.append(ev)
+        one_step(None)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     elapsed = t1 - t0
     if int(flag.item()) != 0:
         print("warning: overflow flag set during the benchmark", file=sys.stderr)
+
+    # Per-pass and per-launch figures: the same number of steps again, with
+    # HIP events around every pass (not part of `value`).
+    use_ev = not args.no_events
+    ev_steps = []
+    if use_ev:
+        for _ in range(args.steps):
+            ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in bufs]
+            one_step(ev)
+            ev_steps.append(ev)
+        torch.cuda.synchronize()
 
     step_flops = sum(L.flops() * (3 if L.dgrad else 2) for L in layers)
     value = step_flops * args.steps / elapsed / 1e12
@@ -461,7 +475,7 @@ def main():
     if depthwise:  # bound by HBM: report the compulsory bytes moved per second
         value = step_bytes * args.steps / elapsed / 1e9
 
-    # per-pass time from the events inside the timed steps
+    # per-pass time from the event-instrumented steps
     pass_ms = {"fwd": 0.0, "dgrad": 0.0, "wgrad": 0.0}
     pass_flops = {"fwd": 0, "dgrad": 0, "wgrad": 0}
     pass_launch_units = {"fwd": 0, "dgrad": 0, "wgrad": 0}

@@ -21,7 +21,7 @@ import numpy as np
 import pytest
 
 import oracle.oracle as orc
-from gpu_util import TOL, Case, full_parity, nchw_f64, oracle_conv, run_gpu, torch
+from gpu_util import TOL, Case, full_parity, nchw_f64, oracle_conv, run_gpu, to_dev, torch
 from paper_2102_06725_amd import inputs as I
 from paper_2102_06725_amd import nnconv as nc
 
@@ -178,3 +178,66 @@ def test_sweep_layer_batch3_full(name, case):
     passes = ("fwd", "dgrad", "wgrad") if case.layer.dgrad else ("fwd", "wgrad")
     errs = full_parity(case, passes=passes)
     print(name, {k: "%.3e" % v for k, v in errs.items()})
+
+
+def test_operand_of_2_gib_takes_the_direct_path():
+    """Maximum size: x of exactly 2 GiB (1 x 128 x 128 x 65536 fp16,
+    channel-last) is past the byte range the fast kernels address with
+    32-bit buffer offsets, so all three passes run on the direct kernels,
+    which index with 64 bits.  Sampled outputs against the oracle applied to
+    gathered sub-problems: a 1x1 stride-1 convolution is pointwise in space
+    (y and dx at a pixel depend only on that pixel's channel column), and
+    dw[k][c] depends only on input channel c and output channel k."""
+    tt = torch()
+    L = I.Layer("x2gib", 1, 65536, 128, 128, 8, 1, 1)
+    case = Case(L, layout="nhwc", dtype=I.F16, loss_scale=1.0, x_kind="absnormal", dy_std=1.0,
+                cfg=91)
+    t = case.tensors()
+    assert t["x"].nbytes == 2 ** 31
+    d = case.desc()
+    s = tt.cuda.current_stream().cuda_stream
+    x, w, dy = to_dev(t["x"]), to_dev(t["w"]), to_dev(t["dy"])
+    y = tt.empty(L.n * L.p * L.q * L.k, dtype=tt.int16, device="cuda")
+    dx = tt.empty(L.n * L.h * L.w * L.c, dtype=tt.int16, device="cuda")
+    dw = tt.empty(L.k * L.c, dtype=tt.float32, device="cuda")
+    for p_, call in ((nc.NNCONV_FWD, lambda ws, nb: nc.nnconv_fwd(
+                         d, x.data_ptr(), w.data_ptr(), y.data_ptr(), 1.0, ws, nb, s)),
+                     (nc.NNCONV_DGRAD, lambda ws, nb: nc.nnconv_dgrad(
+                         d, dy.data_ptr(), w.data_ptr(), dx.data_ptr(), 1.0, ws, nb, s)),
+                     (nc.NNCONV_WGRAD, lambda ws, nb: nc.nnconv_wgrad(
+                         d, x.data_ptr(), dy.data_ptr(), dw.data_ptr(), nc.NNCONV_F32, 1.0, 0,
+                         None, ws, nb, s))):
+        st, nb = nc.nnconv_workspace_size(d, p_)
+        nc.check(st, "workspace_size")
+        ws = tt.empty(max(nb, 1), dtype=tt.uint8, device="cuda")
+        nc.check(call(ws.data_ptr(), nb), "pass %d" % p_)
+        tt.cuda.synchronize()
+        del ws
+    rng = np.random.default_rng(2 ** 31)
+    pix = np.unique(np.concatenate([[0, 127, 128 * 127, 128 * 128 - 1],
+                                    rng.integers(0, 128 * 128, size=28)]))
+    ph, pq = pix // 128, pix % 128
+    wf = I.from_bits(np.ascontiguousarray(t["w"].reshape(L.k, L.c)), I.F16).reshape(L.k, L.c, 1, 1)
+    tol = TOL[I.F16]
+
+    xs = I.from_bits(np.ascontiguousarray(t["x"][0, ph, pq, :]), I.F16)          # (S, C)
+    sub = orc.Conv(len(pix), L.c, 1, 1, L.k, 1, 1, (1, 1), (0, 0), (1, 1), 1)
+    ref = sub.fwd(xs.reshape(len(pix), L.c, 1, 1), wf).reshape(len(pix), L.k)
+    got = y.view(L.p, L.q, L.k)[tt.from_numpy(ph).cuda(), tt.from_numpy(pq).cuda()]
+    got = I.from_bits(got.cpu().numpy().view(np.uint16), I.F16)
+    assert sampled_rel_err(got, ref) <= tol
+
+    dys = I.from_bits(np.ascontiguousarray(t["dy"][0, ph, pq, :]), I.F16)        # (S, K)
+    ref = sub.dgrad(dys.reshape(len(pix), L.k, 1, 1), wf).reshape(len(pix), L.c)
+    got = dx.view(L.h, L.w, L.c)[tt.from_numpy(ph).cuda(), tt.from_numpy(pq).cuda()]
+    got = I.from_bits(got.cpu().numpy().view(np.uint16), I.F16)
+    assert sampled_rel_err(got, ref) <= tol
+
+    chans = np.unique(np.concatenate([[0, L.c - 1], rng.integers(0, L.c, size=14)]))
+    dyall = I.from_bits(np.ascontiguousarray(t["dy"][0].transpose(2, 0, 1)), I.F16)  # (K, H, W)
+    sub1 = orc.Conv(1, 1, L.h, L.w, L.k, 1, 1, (1, 1), (0, 0), (1, 1), 1)
+    dwall = dw.view(L.k, L.c).cpu().numpy().astype(np.float64)
+    for c in chans:
+        xc = I.from_bits(np.ascontiguousarray(t["x"][0, :, :, c]), I.F16)
+        ref = sub1.wgrad(xc.reshape(1, 1, L.h, L.w), dyall.reshape(1, L.k, L.h, L.w), 1.0)
+        assert sampled_rel_err(dwall[:, c], ref.reshape(L.k)) <= tol, "channel %d" % c

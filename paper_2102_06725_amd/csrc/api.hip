@@ -15,6 +15,9 @@ namespace {
 struct Geom {
     int64_t n, c, h, w, k, r, s, sh, sw, ph, pw, dh, dw, g, p, q, cg, kg;
     int layout, dtype;
+    // 1: the 64x64 per-tap weight blocks are block-diagonal in 32x32 blocks
+    // (super-groups of groups of at most 32 channels)
+    int diag32;
 };
 
 constexpr int64_t MAX_ELEMS = int64_t(1) << 40;
@@ -49,6 +52,7 @@ nnconv_status validate(const nnconv_desc *d, Geom *G) {
         return NNCONV_ERR_INVALID_ARG;
     g.layout = d->layout;
     g.dtype = d->dtype;
+    g.diag32 = 0;
     *G = g;
     return NNCONV_OK;
 }
@@ -111,7 +115,16 @@ Geom sg_geom(const Geom &G) {
     Geom S = G;
     S.g = G.c / SUPER_GROUP;
     S.cg = S.kg = SUPER_GROUP;
+    S.diag32 = G.cg <= 32;  // always: the group size divides 64 and is below it
     return S;
+}
+
+// The 64-channel-slice tile for a GEMM with ncols output columns: the
+// block-diagonal variant of the 64-column tile when the weights allow it.
+C64Config pick_c64(int64_t m, int64_t ncols, int64_t red);
+C64Config pick_c64_geom(const Geom &G, int64_t m, int64_t ncols, int64_t red) {
+    const C64Config c = pick_c64(m, ncols, red);
+    return (G.diag32 && ncols == SUPER_GROUP && c == C64S_128x64) ? C64D_128x64 : c;
 }
 
 // ---------------------------------------------------------------------------
@@ -458,7 +471,7 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     if (G.cg % 64 == 0) {
         p.nphase = 1;
         p.ph[0] = phase_of(p.M, p.mi, p.mj, 0, 0, 0, t);
-        return hip_status(launch_igemm_c64(G.dtype, pick_c64(p.M, G.kg, (int64_t)t * G.cg), p,
+        return hip_status(launch_igemm_c64(G.dtype, pick_c64_geom(G, p.M, G.kg, (int64_t)t * G.cg), p,
                                            G.ph > 0 || G.pw > 0, st));
     }
     return hip_status(launch_igemm_c8(G.dtype, pick_c8(G.kg), p, st));
@@ -530,7 +543,7 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
         }
         if (p.nphase == 0) return NNCONV_OK;
         return hip_status(
-            launch_igemm_c64(G.dtype, pick_c64(rows, G.cg, max_red), p, pad, st));
+            launch_igemm_c64(G.dtype, pick_c64_geom(G, rows, G.cg, max_red), p, pad, st));
     }
     // Otherwise sigma_h * sigma_w launches, one per output phase (h mod
     // sigma_h, w mod sigma_w): within a phase every pixel sees the same set of
@@ -554,7 +567,7 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             if (G.kg % 64 == 0) {
                 p.nphase = 1;
                 p.ph[0] = phase_of(p.M, mi, mj, phh, phw, 0, t);
-                TRY_HIP(launch_igemm_c64(G.dtype, pick_c64(p.M, G.cg, (int64_t)t * G.kg), p, pad,
+                TRY_HIP(launch_igemm_c64(G.dtype, pick_c64_geom(G, p.M, G.cg, (int64_t)t * G.kg), p, pad,
                                          st));
             } else {
                 TRY_HIP(launch_igemm_c8(G.dtype, pick_c8(G.cg), p, st));

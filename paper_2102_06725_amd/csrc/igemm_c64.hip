@@ -79,7 +79,12 @@ __device__ __forceinline__ int slot(int r, int c) {
 
 }  // namespace c64
 
-template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool PAD>
+// DIAG: the per-tap 64x64 weight blocks of every 64-column group are
+// block-diagonal in 32x32 blocks (grouped convolution run as 64-channel
+// super-groups, groups of at most 32 channels), so a wave's 32 output
+// columns meet only the matching 32 reduction channels of each 64-channel
+// slice: two of its four k-steps.
+template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool PAD, bool DIAG>
 __global__ __launch_bounds__(WM * WN * 64, (WM * WN == 4) ? ((BM * BN <= 128 * 128) ? 4 : 2) : 1)
 void igemm_c64_kernel(const TNParams P) {
     using namespace c64;
@@ -94,6 +99,7 @@ void igemm_c64_kernel(const TNParams P) {
     constexpr int STAGE_SLOTS = A_SLOTS + B_SLOTS;
     constexpr int LOADS = A_LD + B_LD;
     static_assert(FM >= 1 && FN >= 1 && A_LD >= 1 && B_LD >= 1, "tile shape");
+    static_assert(!DIAG || (FN == 1 && WTN == 32 && BKC == 8), "block-diagonal: 32-column waves");
 
     constexpr int LDS_SLOTS = STAGES * STAGE_SLOTS > BM * BN / 8 ? STAGES * STAGE_SLOTS : BM * BN / 8;
     __shared__ u32x4 lds[LDS_SLOTS];
@@ -212,6 +218,23 @@ void igemm_c64_kernel(const TNParams P) {
     const int k_iters = ntaps * (P.cr / BK);
 
     auto compute = [&](const u32x4 *st) {
+        if constexpr (DIAG) {
+            // k-steps 2h, 2h+1 carry the reduction channels 32h .. 32h+31 of
+            // the slice, h = the half of the 64-column group the wave's
+            // columns lie in
+            const int h = (wn * WTN / 32) & 1;
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int kc = 2 * (2 * h + kk) + khalf;
+                u32x4 fp[FM];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) fp[i] = st[slot<BKC>(wm * WTM + i * 32 + l32, kc)];
+                const u32x4 fw = st[A_SLOTS + slot<BKC>(wn * WTN + l32, kc)];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) acc[0][i] = mfma32<T>(fw, fp[i], acc[0][i]);
+            }
+            return;
+        }
 #pragma unroll
         for (int ks = 0; ks < BKC / 2; ++ks) {
             const int kc = 2 * ks + khalf;
@@ -306,7 +329,7 @@ void igemm_c64_kernel(const TNParams P) {
     }
 }
 
-template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES>
+template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool DIAG = false>
 static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
     p.tiles_n = (p.ncols + BN - 1) / BN;
     int64_t nb = 0;
@@ -318,10 +341,10 @@ static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (pad)
-        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, true>),
+        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, true, DIAG>),
                            dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     else
-        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, false>),
+        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, false, DIAG>),
                            dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
@@ -334,7 +357,8 @@ static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
 //            workgroups per CU)
 // Single-stage tiles, whose small LDS footprint lets 3-5 workgroups share a
 // CU and cover each other's load latency:
-//   128x128: 4 waves of 64x64 (32 KB);  128x64: 4 waves of 64x32 (24 KB)
+//   128x128: 4 waves of 64x64 (32 KB);  128x64: 4 waves of 64x32 (24 KB),
+//   also with block-diagonal 32x32 weight blocks (half the k-steps)
 template <class T>
 static hipError_t launch_c64_t(C64Config cfg, TNParams &p, bool pad, hipStream_t st) {
     switch (cfg) {
@@ -342,6 +366,7 @@ static hipError_t launch_c64_t(C64Config cfg, TNParams &p, bool pad, hipStream_t
         case C64W_256x256: return launch_c64_cfg<T, 256, 256, 4, 4, 8, 2>(p, pad, st);
         case C64_128x128: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 2>(p, pad, st);
         case C64S_128x64: return launch_c64_cfg<T, 128, 64, 2, 2, 8, 1>(p, pad, st);
+        case C64D_128x64: return launch_c64_cfg<T, 128, 64, 2, 2, 8, 1, true>(p, pad, st);
         case C64S_128x128:
         default: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 1>(p, pad, st);
     }

@@ -87,7 +87,9 @@ enum C64Config { C64_256x256 = 0,   // 8 waves, 64-element slices, 2 stages
                  C64_128x128 = 1,   // 4 waves, 64-element slices, 2 stages
                  C64S_128x128 = 2,  // single stage (several workgroups per CU)
                  C64S_128x64 = 3,
-                 C64W_256x256 = 4 };  // 16 waves of 64x64, 2 stages
+                 C64W_256x256 = 4,    // 16 waves of 64x64, 2 stages
+                 C64D_128x64 = 5 };   // C64S_128x64 for block-diagonal 64x64 weights
+                                      // (32x32 blocks): half the k-steps per wave
 hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hipStream_t st);
 
 // Forward pass for 8-channel (16-byte) channel-last pixels, 64 output

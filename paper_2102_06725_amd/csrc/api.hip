@@ -160,7 +160,7 @@ WGConfig pick_wg(int64_t kg, int64_t rscg) {
 }
 
 int64_t wg_target_blocks(WGConfig cfg) {
-    return cfg == WG_64x128 ? 1024 : cfg == WG_256x256 ? 256 : 512;
+    return (cfg == WG_64x128 || cfg == WG_64x128D) ? 1024 : cfg == WG_256x256 ? 256 : 512;
 }
 
 WgPlan plan_wgrad_fast(const Geom &G) {
@@ -175,8 +175,9 @@ WgPlan plan_wgrad_fast(const Geom &G) {
     }
     const int64_t rscg = G.r * G.s * G.cg;
     pl.cfg = pick_wg(G.kg, rscg);
-    static const int64_t tile_m[] = {128, 64, 256, 128};
-    static const int64_t tile_n[] = {128, 128, 256, 128};
+    if (G.diag32 && pl.cfg == WG_64x128 && G.kg == SUPER_GROUP) pl.cfg = WG_64x128D;
+    static const int64_t tile_m[] = {128, 64, 256, 128, 64};
+    static const int64_t tile_n[] = {128, 128, 256, 128, 128};
     const int64_t bmk = tile_m[pl.cfg], bnj = tile_n[pl.cfg];
     const int64_t tiles = G.g * ((G.kg + bmk - 1) / bmk) * ((rscg + bnj - 1) / bnj);
     const int64_t npq = G.n * G.p * G.q;

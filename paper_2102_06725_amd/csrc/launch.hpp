@@ -133,7 +133,8 @@ struct WGParams {
     int32_t tiles_m, tiles_n;   // filled by the launcher
 };
 
-enum WGConfig { WG_128x128 = 0, WG_64x128 = 1, WG_256x256 = 2, WG_128x128S = 3 };
+enum WGConfig { WG_128x128 = 0, WG_64x128 = 1, WG_256x256 = 2, WG_128x128S = 3,
+                WG_64x128D = 4 };  // WG_64x128 for block-diagonal super-group gradients
 
 // Pixel ranges of pix_per_split (a multiple of 32) pixels each.
 hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);

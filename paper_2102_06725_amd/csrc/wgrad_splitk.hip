@@ -76,7 +76,12 @@ __device__ __forceinline__ uint32_t tile_off(int p, int co) {
 
 }  // namespace wgs
 
-template <class T, int BM, int BN, int WM, int WN, int BKP, int STAGES>
+// DIAG: block-diagonal super-group gradients (groups of at most 32 channels
+// run as 64-channel super-groups): only the 32x32 blocks whose filter rows
+// and input channels lie in the same half of a 64-channel group are kept by
+// the reduction, so each wave computes and writes only the column block that
+// matches its 32 rows.
+template <class T, int BM, int BN, int WM, int WN, int BKP, int STAGES, bool DIAG>
 __global__ __launch_bounds__(WM * WN * 64, (STAGES * BKP * (BM + BN) * 2 > 80 * 1024) ? 1
                                            : (STAGES * BKP * (BM + BN) * 2 > 40 * 1024) ? 2
                                                                                        : 4)
@@ -94,6 +99,10 @@ void wgrad_splitk_kernel(const WGParams P) {
     static_assert(A_LD >= 1 && B_LD >= 1 && FM >= 1 && FN >= 1, "tile shape");
     static_assert(AROWB >= 128 && BROWB >= 128, "rows of at least two 64-byte segments");
     static_assert(BKP % 16 == 0, "pixel slice");
+    static_assert(!DIAG || (FM == 1 && WTM == 32 && FN == 2 && WTN == 64 && BM % 64 == 0 &&
+                            BN % 64 == 0),
+                  "block-diagonal: 32-row waves over 64-column pairs");
+    constexpr int FNA = DIAG ? 1 : FN;  // accumulated 32-column blocks per wave
 
     __shared__ u32x4 lds[STAGES * STAGE_BYTES / 16];
 
@@ -188,11 +197,14 @@ void wgrad_splitk_kernel(const WGParams P) {
         }
     };
 
-    f32x16 acc[FM][FN];
+    f32x16 acc[FM][FNA];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = f32x16{};
+        for (int j = 0; j < FNA; ++j) acc[i][j] = f32x16{};
+    // DIAG: the wave's rows are half wm % 2 of a 64-row group; its column
+    // block is the one with the same half of each 64-channel tap block
+    const int dcol = DIAG ? wn * WTN + (wm & 1) * 32 : 0;
 
     // fragment reads: lane group gq = lane/16 covers channels 16*(gq%2) of a
     // 32-wide block and pixels 8*(gq/2) of the 16-pixel k-step
@@ -223,15 +235,16 @@ void wgrad_splitk_kernel(const WGParams P) {
         const char *st = (const char *)&lds[0] + buf * STAGE_BYTES;
 #pragma unroll
         for (int ks = 0; ks < BKP / 16; ++ks) {
-            u32x4 fa[FM], fb[FN];
+            u32x4 fa[FM], fb[FNA];
 #pragma unroll
             for (int i = 0; i < FM; ++i) fa[i] = frag(st, 1, ks, wm * WTM + i * 32);
 #pragma unroll
-            for (int j = 0; j < FN; ++j) fb[j] = frag(st + A_BYTES, 0, ks, wn * WTN + j * 32);
+            for (int j = 0; j < FNA; ++j)
+                fb[j] = frag(st + A_BYTES, 0, ks, DIAG ? dcol : wn * WTN + j * 32);
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = mfma32<T>(fa[i], fb[j], acc[i][j]);
+                for (int j = 0; j < FNA; ++j) acc[i][j] = mfma32<T>(fa[i], fb[j], acc[i][j]);
         }
     };
     if constexpr (STAGES == 1) {
@@ -263,8 +276,8 @@ void wgrad_splitk_kernel(const WGParams P) {
     const int K = P.kg * P.groups;
     float *ws = P.ws + (int64_t)split * K * P.rscg;
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int col = j0 + wn * WTN + j * 32 + l32;
+    for (int j = 0; j < FNA; ++j) {
+        const int col = DIAG ? j0 + dcol + l32 : j0 + wn * WTN + j * 32 + l32;
         if (col >= P.rscg) continue;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
@@ -277,20 +290,21 @@ void wgrad_splitk_kernel(const WGParams P) {
     }
 }
 
-template <class T, int BM, int BN, int WM, int WN, int BKP, int STAGES>
+template <class T, int BM, int BN, int WM, int WN, int BKP, int STAGES, bool DIAG = false>
 static hipError_t launch_wgs(WGParams &p, hipStream_t st) {
     p.tiles_m = (p.kg + BM - 1) / BM;
     p.tiles_n = (p.rscg + BN - 1) / BN;
     const int64_t nb = (int64_t)p.tiles_m * p.tiles_n * p.splits * p.groups;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((wgrad_splitk_kernel<T, BM, BN, WM, WN, BKP, STAGES>), dim3((uint32_t)nb),
+    hipLaunchKernelGGL((wgrad_splitk_kernel<T, BM, BN, WM, WN, BKP, STAGES, DIAG>), dim3((uint32_t)nb),
                        dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
 
 // Configurations (LDS per workgroup):
-//    64x128: 4 waves of 32x64, 64-pixel slices, single stage (24 KB)
+//    64x128: 4 waves of 32x64, 64-pixel slices, single stage (24 KB); also
+//            block-diagonal (each wave one 32x32 block)
 //   128x128: 8 waves of 64x32, 64-pixel slices, 2 stages (64 KB; two
 //            workgroups per CU)
 //   128x128 single stage: 4 waves of 64x64, 64-pixel slices (32 KB; four
@@ -303,6 +317,7 @@ template <class T>
 static hipError_t launch_wgs_t(WGConfig cfg, WGParams &p, hipStream_t st) {
     switch (cfg) {
         case WG_64x128: return launch_wgs<T, 64, 128, 2, 2, 64, 1>(p, st);
+        case WG_64x128D: return launch_wgs<T, 64, 128, 2, 2, 64, 1, true>(p, st);
         case WG_256x256: return launch_wgs<T, 256, 256, 4, 4, 32, 2>(p, st);
         case WG_128x128S: return launch_wgs<T, 128, 128, 2, 2, 64, 1>(p, st);
         case WG_128x128:

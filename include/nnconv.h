@@ -30,6 +30,8 @@
  *     by nnconv_workspace_size) and never synchronises.
  *   - Work is queued on the caller's HIP stream (hipStream_t passed as
  *     void*; NULL means the default stream).  Calls return once queued.
+ *     They queue kernel launches only (no memset, copy or event), so a
+ *     sequence of calls may be captured into a HIP graph and replayed.
  *   - The library keeps no mutable global state: calls are reentrant, and
  *     calls on different streams with disjoint buffers may run concurrently.
  *   - Fast (matrix-core) paths need 16-byte aligned pointers and Cg, Kg that

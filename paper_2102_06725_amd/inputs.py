@@ -39,7 +39,8 @@ def to_bits(v: np.ndarray, dtype: str) -> np.ndarray:
     """Round-to-nearest-even quantisation of float values to fp16 or bf16,
     returned as raw uint16 bit patterns."""
     if dtype == F16:
-        return np.asarray(v).astype(np.float16).view(np.uint16)
+        with np.errstate(over="ignore"):  # values past the fp16 range round to +-inf
+            return np.asarray(v).astype(np.float16).view(np.uint16)
     if dtype == BF16:
         f = np.ascontiguousarray(v, dtype=np.float32)
         b = f.view(np.uint32).astype(np.uint64)

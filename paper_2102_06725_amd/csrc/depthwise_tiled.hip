@@ -646,7 +646,9 @@ int wg_gmax(int r, int cbv) { return 256 / (cbv * r); }
 
 // Backward-weight tiling: per CBV, dy rows per tile balanced over the image
 // height (at most GMAX); the CBV with the fewest (channel block, tile) pairs.
-// Splits: about 2048 workgroups.
+// Splits: about 1024 workgroups (four per compute unit); more splits cost more
+// than the extra parallelism gives, since each workgroup then walks too few tiles
+// to hide its prefetch.
 DWWgPlan plan_wgrad(const DWParams &p) {
     DWWgPlan pl;
     const int tw = p.sh == 1 ? 8 : 4;
@@ -674,7 +676,7 @@ DWWgPlan plan_wgrad(const DWParams &p) {
         pl.tiles_per_split = 0;
         return pl;
     }
-    int64_t splits = 2048 / pl.cblocks;
+    int64_t splits = 1024 / pl.cblocks;
     if (splits < 1) splits = 1;
     if (splits > ntiles) splits = ntiles;
     if (splits > 65535) splits = 65535;

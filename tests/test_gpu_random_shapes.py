@@ -10,8 +10,10 @@ are capped so that the oracle takes well under a second per case."""
 import numpy as np
 import pytest
 
-from gpu_util import Case, full_parity, torch
+import oracle.oracle as orc
+from gpu_util import TOL, Case, full_parity, nchw_f64, oracle_conv, run_gpu, to_nchw, torch
 from paper_2102_06725_amd import inputs as I
+from paper_2102_06725_amd import nnconv as nc
 
 pytestmark = pytest.mark.gpu
 
@@ -92,3 +94,42 @@ def _setup(nnlib, oracle_lib):
 def test_random_shape_parity(case):
     print("case:", _id(case), flush=True)
     full_parity(case)
+
+
+WG_CASES = CASES[::3]
+
+
+@pytest.mark.parametrize("case", WG_CASES, ids=[_id(c) for c in WG_CASES])
+def test_random_wgrad_output_modes(case):
+    """Backward-weight with the other output modes on the same geometries:
+    dw in fp32 or in the operand dtype, written (beta = 0) or added to a
+    previous dw (beta = 1), against the oracle's beta*dw_old + sum/S from the
+    exact values the GPU was given."""
+    print("case:", _id(case), flush=True)
+    L = case.layer
+    cg = L.c // L.groups
+    rng = np.random.default_rng(SEED + 1000 + case.layer_id)
+    half = bool(rng.integers(0, 2))
+    beta = int(rng.integers(0, 2))
+    t = case.tensors()
+    x, w, dy = nchw_f64(case, t)
+    old = rng.standard_normal((L.k, cg, L.r, L.s)).astype(np.float32)   # [K][Cg][R][S]
+    old_lay = old if case.layout == "nchw" else old.transpose(0, 2, 3, 1)
+    if half:
+        dw_old = I.to_bits(np.ascontiguousarray(old_lay), case.dtype)
+        old_ref = I.from_bits(dw_old, case.dtype)
+        if case.layout == "nhwc":
+            old_ref = old_ref.transpose(0, 3, 1, 2)
+        dw_dtype = nc.NNCONV_F16 if case.dtype == I.F16 else nc.NNCONV_BF16
+    else:
+        dw_old = np.ascontiguousarray(old_lay)
+        old_ref = old.astype(np.float64)
+        dw_dtype = nc.NNCONV_F32
+    got = run_gpu(case, t, passes=("wgrad",), dw_dtype=dw_dtype, accumulate=beta,
+                  dw_old=dw_old if beta else None)
+    ref = oracle_conv(case).wgrad(x, dy, 1.0 / case.loss_scale, beta=beta,
+                                  dw_old=old_ref if beta else None)
+    g = to_nchw(case, "dw", got["dw"])
+    assert np.all(np.isfinite(g))
+    tol = TOL[case.dtype] if half else 1e-4
+    assert orc.rel_err(g, ref) <= tol, (half, beta)

@@ -49,6 +49,14 @@
  *     the matrix-core kernels.  Results for finite inputs are those of the
  *     grouped convolution; a non-finite input value also makes the outputs
  *     of the other groups sharing its 64-channel block NaN.
+ *   - Non-finite inputs: forward and backward-weight multiply the zeros of
+ *     the zero-extended input at taps outside the image, as the definition
+ *     reads, so an inf or NaN weight (forward) or dy (backward-weight) makes
+ *     every sum it meets non-finite, padding included.  Backward-data on
+ *     the matrix-core and depthwise kernels reads dy zero-extended at every
+ *     tap, so a non-finite weight also makes dx non-finite at positions the
+ *     definition does not reach from that tap; the direct kernels add only
+ *     the taps the definition has.
  *
  * Errors: every argument check happens on the host before anything is
  * queued.  On a non-OK status nothing is launched and no output or

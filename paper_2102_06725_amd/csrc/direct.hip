@@ -27,16 +27,21 @@ __global__ __launch_bounds__(256) void direct_fwd_kernel(const DirectParams P, c
     const int k = (int)(f % P.k); f /= P.k;
     const int n = (int)f;
     const int g = k / P.kg;
+    // Taps outside the image multiply the zero of the zero-extended input
+    // rather than being skipped, so a non-finite weight gives a non-finite
+    // output there too, as the definition does (and as the kernels whose
+    // range-checked loads return zeros do).
     float acc = 0.f;
     for (int c = 0; c < P.cg; ++c) {
         const int ci = g * P.cg + c;
         for (int r = 0; r < P.r; ++r) {
             const int h = p * P.sh - P.ph + r * P.dh;
-            if (h < 0 || h >= P.h) continue;
+            const bool hin = h >= 0 && h < P.h;
             for (int s = 0; s < P.s; ++s) {
                 const int wv = q * P.sw - P.pw + s * P.dw;
-                if (wv < 0 || wv >= P.w) continue;
-                const float xv = ld16<T>(x, n * P.xs[0] + ci * P.xs[1] + h * P.xs[2] + wv * P.xs[3]);
+                const bool in = hin && wv >= 0 && wv < P.w;
+                const float xv =
+                    in ? ld16<T>(x, n * P.xs[0] + ci * P.xs[1] + h * P.xs[2] + wv * P.xs[3]) : 0.f;
                 const float fv = ld16<T>(w, k * P.wsd[0] + c * P.wsd[1] + r * P.wsd[2] + s * P.wsd[3]);
                 acc += xv * fv;
             }
@@ -109,8 +114,11 @@ __global__ __launch_bounds__(256) void direct_wgrad_kernel(const DirectParams P,
         const int p = rm / P.q, q = rm - (rm / P.q) * P.q;
         const int h = p * P.sh - P.ph + r * P.dh;
         const int wv = q * P.sw - P.pw + s * P.dw;
-        if (h < 0 || h >= P.h || wv < 0 || wv >= P.w) continue;
-        const float xv = ld16<T>(x, n * P.xs[0] + ci * P.xs[1] + h * P.xs[2] + wv * P.xs[3]);
+        // outside the image: the zero of the zero-extended input, multiplied
+        // (a non-finite dy then makes the sum non-finite, as defined)
+        const bool in = h >= 0 && h < P.h && wv >= 0 && wv < P.w;
+        const float xv =
+            in ? ld16<T>(x, n * P.xs[0] + ci * P.xs[1] + h * P.xs[2] + wv * P.xs[3]) : 0.f;
         const float dv = ld16<T>(dy, n * P.ys[0] + k * P.ys[1] + p * P.ys[2] + q * P.ys[3]);
         acc += dv * xv;
     }

@@ -133,3 +133,29 @@ def test_random_wgrad_output_modes(case):
     assert np.all(np.isfinite(g))
     tol = TOL[case.dtype] if half else 1e-4
     assert orc.rel_err(g, ref) <= tol, (half, beta)
+
+
+FLAG_CASES = CASES[::5]
+INF_BITS = {I.F16: 0x7C00, I.BF16: 0x7F80}
+
+
+@pytest.mark.parametrize("case", FLAG_CASES, ids=[_id(c) for c in FLAG_CASES])
+def test_random_overflow_flag(case):
+    """The overflow flag on every dispatch path: clear after a clean
+    backward-weight, set when one dy element is +inf (that output channel's
+    dw sums become inf or NaN, as inf * 0 is NaN)."""
+    print("case:", _id(case), flush=True)
+    tt = torch()
+    rng = np.random.default_rng(SEED + 2000 + case.layer_id)
+    dw_dtype = nc.NNCONV_F32 if rng.integers(0, 2) else (
+        nc.NNCONV_F16 if case.dtype == I.F16 else nc.NNCONV_BF16)
+    t = case.tensors()
+    flag = tt.zeros(1, dtype=tt.int32, device="cuda")
+    run_gpu(case, t, passes=("wgrad",), dw_dtype=dw_dtype, flag=flag)
+    assert int(flag.item()) == 0, "flag set on finite inputs"
+    bad = dict(t)
+    dy = np.array(t["dy"], copy=True)
+    dy.reshape(-1)[int(rng.integers(0, dy.size))] = INF_BITS[case.dtype]
+    bad["dy"] = dy
+    run_gpu(case, bad, passes=("wgrad",), dw_dtype=dw_dtype, flag=flag)
+    assert int(flag.item()) == 1, "flag not set with an inf in dy"

@@ -159,3 +159,43 @@ def test_random_overflow_flag(case):
     bad["dy"] = dy
     run_gpu(case, bad, passes=("wgrad",), dw_dtype=dw_dtype, flag=flag)
     assert int(flag.item()) == 1, "flag not set with an inf in dy"
+
+
+NF_CASES = CASES[2::5]
+
+
+def _super_group(case):
+    L = case.layer
+    return 1 < L.groups < L.c and L.c == L.k and L.c % 64 == 0 and (L.c // L.groups) < 64
+
+
+@pytest.mark.parametrize("case", NF_CASES, ids=[_id(c) for c in NF_CASES])
+def test_random_nonfinite_forward(case):
+    """Where a non-finite operand reaches in the forward pass: one +inf in x,
+    then one in w; the outputs that are not finite (none if the pixel is
+    never read) are those of the oracle
+    (which multiplies the padding zeros, 0 * inf = NaN).  Super-groups run
+    64-channel blocks with zero weights between groups, which may only add
+    NaNs inside the block that holds the bad value."""
+    print("case:", _id(case), flush=True)
+    rng = np.random.default_rng(SEED + 3000 + case.layer_id)
+    t = case.tensors()
+    cv = oracle_conv(case)
+    for which in ("x", "w"):
+        bad = dict(t)
+        a = np.array(t[which], copy=True)
+        a.reshape(-1)[int(rng.integers(0, a.size))] = INF_BITS[case.dtype]
+        bad[which] = a
+        got = run_gpu(case, bad, passes=("fwd",))
+        g = to_nchw(case, "y", got["y"])
+        x, w, _ = nchw_f64(case, bad)
+        with np.errstate(invalid="ignore", over="ignore"):
+            ref = cv.fwd(x, w)
+        want, have = ~np.isfinite(ref), ~np.isfinite(g)
+        # every output of the channel meets the bad weight; a strided or
+        # dilated forward may never read the bad input pixel
+        assert which == "x" or want.any()
+        if _super_group(case):
+            assert np.all(have[want]), which
+        else:
+            assert np.array_equal(have, want), which

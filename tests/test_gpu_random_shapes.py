@@ -199,3 +199,31 @@ def test_random_nonfinite_forward(case):
             assert np.all(have[want]), which
         else:
             assert np.array_equal(have, want), which
+
+
+@pytest.mark.parametrize("case", NF_CASES, ids=[_id(c) for c in NF_CASES])
+def test_random_nonfinite_dgrad(case):
+    """Backward-data with one +inf in dy: the non-finite dx are the oracle's
+    (super-groups: at least those).  With one +inf in w the matrix-core and
+    depthwise kernels, which read dy zero-extended at every tap, may also
+    make dx non-finite where the definition has no term with that weight, so
+    there the oracle's non-finite dx only have to be covered."""
+    print("case:", _id(case), flush=True)
+    rng = np.random.default_rng(SEED + 4000 + case.layer_id)
+    t = case.tensors()
+    cv = oracle_conv(case)
+    for which in ("dy", "w"):
+        bad = dict(t)
+        a = np.array(t[which], copy=True)
+        a.reshape(-1)[int(rng.integers(0, a.size))] = INF_BITS[case.dtype]
+        bad[which] = a
+        got = run_gpu(case, bad, passes=("dgrad",))
+        g = to_nchw(case, "dx", got["dx"])
+        _, w, dy = nchw_f64(case, bad)
+        with np.errstate(invalid="ignore", over="ignore"):
+            ref = cv.dgrad(dy, w)
+        want, have = ~np.isfinite(ref), ~np.isfinite(g)
+        if which == "dy" and not _super_group(case):
+            assert np.array_equal(have, want), which
+        else:
+            assert np.all(have[want]), which

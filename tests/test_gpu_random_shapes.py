@@ -5,7 +5,8 @@ these draw combinations nobody picked: layout, dtype, loss scale, filter
 size, stride, padding, dilation, group structure and ragged image sizes,
 from five families that between them reach every dispatch path (8-channel
 and 64-channel implicit GEMMs with their stride phases, the direct kernels,
-the tiled and gather depthwise kernels, and 64-channel super-groups).  Sizes
+the tiled and gather depthwise kernels, and 64-channel super-groups), with
+alpha != 1 on about a third of them.  Sizes
 are capped so that the oracle takes well under a second per case."""
 import numpy as np
 import pytest
@@ -56,6 +57,7 @@ def _draw(rng, i):
 
 def _cases():
     rng = np.random.default_rng(SEED)
+    rng_alpha = np.random.default_rng(SEED + 7)   # alpha of fwd / dgrad
     out = []
     i = 0
     while len(out) < N_CASES:
@@ -68,8 +70,9 @@ def _cases():
         layout = "nchw" if rng.random() < 0.3 else "nhwc"
         dtype = I.BF16 if rng.random() < 0.35 else I.F16
         scale = float(rng.choice([1.0, 128.0, 1024.0]))
+        alpha = 1.0 if rng_alpha.random() < 0.7 else float(rng_alpha.choice([0.5, 2.0, 0.3, -1.0]))
         out.append(Case(L, layout=layout, dtype=dtype, loss_scale=scale, cfg=93,
-                        layer_id=len(out)))
+                        layer_id=len(out), alpha=alpha))
     return out
 
 
@@ -78,9 +81,9 @@ CASES = _cases()
 
 def _id(c):
     L = c.layer
-    return "%s n%d c%d %dx%d k%d r%ds%d st%d p%d d%d g%d %s %s" % (
+    return "%s n%d c%d %dx%d k%d r%ds%d st%d p%d d%d g%d %s %s a%g" % (
         L.name, L.n, L.c, L.h, L.w, L.k, L.r, L.s, L.stride, L.pad, L.dil, L.groups, c.layout,
-        c.dtype)
+        c.dtype, c.alpha)
 
 
 @pytest.fixture(scope="module", autouse=True)

@@ -30,6 +30,21 @@ def to_dev(bits: np.ndarray):
     return t.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to("cuda")
 
 
+class Shifted:
+    """16-bit input bits on the device starting `shift` elements past a
+    16-byte aligned allocation (data_ptr() is the shifted address)."""
+
+    def __init__(self, bits: np.ndarray, shift: int):
+        flat = np.ascontiguousarray(bits).view(np.int16).ravel()
+        host = np.zeros(flat.size + shift, np.int16)
+        host[shift:] = flat
+        self.buf = to_dev(host)
+        self.shift = shift
+
+    def data_ptr(self) -> int:
+        return self.buf.data_ptr() + 2 * self.shift
+
+
 class Guarded:
     """A device buffer of `numel` elements with guard bands on both sides."""
 
@@ -129,23 +144,28 @@ def stream():
 
 
 def run_gpu(case: Case, t, passes=("fwd", "dgrad", "wgrad"), dw_dtype=None, inv_scale=None,
-            accumulate=0, dw_old=None, flag=None, dw_shift=0):
+            accumulate=0, dw_old=None, flag=None, dw_shift=0, in_shift=0, out_shift=0):
     """Run the requested passes on the GPU; returns dict of output bits /
-    fp32 values in the case's layout."""
+    fp32 values in the case's layout.  in_shift / out_shift move x, w, dy /
+    y, dx that many 16-bit elements off 16-byte alignment."""
     L = case.layer
     tt = torch()
     d = case.desc()
-    x, w, dy = to_dev(t["x"]), to_dev(t["w"]), to_dev(t["dy"])
+    if in_shift:
+        x, w, dy = (Shifted(t["x"], in_shift), Shifted(t["w"], in_shift),
+                    Shifted(t["dy"], in_shift))
+    else:
+        x, w, dy = to_dev(t["x"]), to_dev(t["w"]), to_dev(t["dy"])
     out = {}
     s = stream()
     if "fwd" in passes:
-        y = Guarded(L.n * L.k * L.p * L.q)
+        y = Guarded(L.n * L.k * L.p * L.q, shift=out_shift)
         ws, nb = workspace(d, nc.NNCONV_FWD)
         nc.check(nc.nnconv_fwd(d, x.data_ptr(), w.data_ptr(), y.ptr(), case.alpha, ws.data_ptr(),
                                nb, s), "fwd")
         out["y"] = y
     if "dgrad" in passes:
-        dx = Guarded(L.n * L.c * L.h * L.w)
+        dx = Guarded(L.n * L.c * L.h * L.w, shift=out_shift)
         ws, nb = workspace(d, nc.NNCONV_DGRAD)
         nc.check(nc.nnconv_dgrad(d, dy.data_ptr(), w.data_ptr(), dx.ptr(), case.alpha,
                                  ws.data_ptr(), nb, s), "dgrad")

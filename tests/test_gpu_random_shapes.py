@@ -230,3 +230,25 @@ def test_random_nonfinite_dgrad(case):
             assert np.array_equal(have, want), which
         else:
             assert np.all(have[want]), which
+
+
+UA_CASES = CASES[4::7]
+
+
+@pytest.mark.parametrize("case", UA_CASES, ids=[_id(c) for c in UA_CASES])
+def test_random_unaligned_operands(case):
+    """Operands one or three 16-bit elements off 16-byte alignment (inputs,
+    outputs and dw) must take kernels that need no alignment and give the
+    oracle's results."""
+    print("case:", _id(case), flush=True)
+    rng = np.random.default_rng(SEED + 5000 + case.layer_id)
+    sh_in, sh_out = int(rng.choice([1, 3])), int(rng.choice([0, 1, 3]))
+    t = case.tensors()
+    got = run_gpu(case, t, in_shift=sh_in, out_shift=sh_out, dw_shift=1)
+    x, w, dy = nchw_f64(case, t)
+    cv = oracle_conv(case)
+    tol = TOL[case.dtype]
+    assert orc.rel_err(to_nchw(case, "y", got["y"]), cv.fwd(x, w, alpha=case.alpha)) <= tol
+    assert orc.rel_err(to_nchw(case, "dx", got["dx"]), cv.dgrad(dy, w, alpha=case.alpha)) <= tol
+    assert orc.rel_err(to_nchw(case, "dw", got["dw"]),
+                       cv.wgrad(x, dy, 1.0 / case.loss_scale)) <= tol

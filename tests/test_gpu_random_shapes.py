@@ -252,3 +252,57 @@ def test_random_unaligned_operands(case):
     assert orc.rel_err(to_nchw(case, "dx", got["dx"]), cv.dgrad(dy, w, alpha=case.alpha)) <= tol
     assert orc.rel_err(to_nchw(case, "dw", got["dw"]),
                        cv.wgrad(x, dy, 1.0 / case.loss_scale)) <= tol
+
+
+def _tf_shapes():
+    rng = np.random.default_rng(SEED + 6000)
+    out = []
+    for i in range(24):
+        mult8 = i % 2 == 0          # half take the 16-byte vector kernels
+        c = 8 * int(rng.integers(1, 12)) if mult8 else int(rng.integers(1, 40))
+        n, h, w = int(rng.integers(1, 4)), int(rng.integers(1, 70)), int(rng.integers(1, 70))
+        if mult8:
+            w = 8 * ((w + 7) // 8)
+        c_pad = c + int(rng.choice([0, 0, 8, 16])) if mult8 else c + int(rng.integers(0, 9))
+        out.append((n, c, h, w, c_pad))
+    return out
+
+
+@pytest.mark.parametrize("shape", _tf_shapes(), ids=lambda s: "n%d c%d %dx%d cp%d" % s)
+def test_random_transforms_bit_exact(shape):
+    """Layout transforms on random sizes, both the 16-byte vector kernels
+    (multiples of 8) and the element ones: NCHW -> NHWC with channel
+    padding, back, channel padding alone, and KCRS <-> KRSC weights, all
+    bit-exact against numpy transposes of random 16-bit patterns."""
+    from gpu_util import Guarded, stream, to_dev
+    tt = torch()
+    n, c, h, w, cp = shape
+    print("shape:", shape, flush=True)
+    rng = np.random.default_rng(SEED + 6100 + c * 131 + h * 7 + w)
+    s = stream()
+    src = rng.integers(0, 65535, size=(n, c, h, w), dtype=np.uint16)
+    ref = np.zeros((n, h, w, cp), np.uint16)
+    ref[..., :c] = src.transpose(0, 2, 3, 1)
+    out = Guarded(n * h * w * cp)
+    nc.check(nc.nnconv_nchw_to_nhwc(to_dev(src).data_ptr(), out.ptr(), n, c, h, w, cp, s))
+    nhwc = np.ascontiguousarray(src.transpose(0, 2, 3, 1))
+    back = Guarded(n * c * h * w)
+    nc.check(nc.nnconv_nhwc_to_nchw(to_dev(nhwc).data_ptr(), back.ptr(), n, c, h, w, s))
+    padded = Guarded(n * h * w * cp)
+    nc.check(nc.nnconv_pad_channels(to_dev(nhwc).data_ptr(), padded.ptr(), n * h * w, c, cp, s))
+    # weights: K = n*3, Cg = c, R x S from h, w
+    k, r, sz = 3 * n, 1 + h % 5, 1 + w % 4
+    wk = rng.integers(0, 65535, size=(k, c, r, sz), dtype=np.uint16)
+    o = Guarded(k * r * sz * cp)
+    nc.check(nc.nnconv_weight_kcrs_to_krsc(to_dev(wk).data_ptr(), o.ptr(), k, c, r, sz, cp, s))
+    o2 = Guarded(wk.size)
+    nc.check(nc.nnconv_weight_krsc_to_kcrs(
+        to_dev(np.ascontiguousarray(wk.transpose(0, 2, 3, 1))).data_ptr(), o2.ptr(), k, c, r, sz, s))
+    tt.cuda.synchronize()
+    assert np.array_equal(out.host().reshape(ref.shape), ref)
+    assert np.array_equal(back.host().reshape(src.shape), src)
+    assert np.array_equal(padded.host().reshape(ref.shape), ref)
+    refw = np.zeros((k, r, sz, cp), np.uint16)
+    refw[..., :c] = wk.transpose(0, 2, 3, 1)
+    assert np.array_equal(o.host().reshape(refw.shape), refw)
+    assert np.array_equal(o2.host().reshape(wk.shape), wk)

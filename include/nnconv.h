@@ -135,6 +135,37 @@ nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, const void *w, 
 nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, const void *w, void *dx,
                            float alpha, void *ws, size_t ws_bytes, void *hip_stream);
 
+/* Tiles of the matrix-core implicit GEMM that runs the forward pass and the
+ * backward-data pass when the reduction channels per filter tap (Cg for the
+ * forward pass, Kg for backward-data) are a multiple of 64.  nnconv_fwd and
+ * nnconv_dgrad pick one per shape; the _tile variants below force one, for
+ * tests that must reach every tile on small shapes and for tuning.  Every
+ * tile computes the same sums (the fp32 summation order may differ). */
+typedef enum {
+    NNCONV_TILE_256x256_8W = 0,   /* 8 waves of 128x64, 2 stages of 64-element slices */
+    NNCONV_TILE_128x128_2S = 1,   /* 4 waves of 64x64, 2 stages */
+    NNCONV_TILE_128x128 = 2,      /* 4 waves of 64x64, single stage */
+    NNCONV_TILE_128x64 = 3,       /* 4 waves of 64x32, single stage */
+    NNCONV_TILE_256x256_16W = 4,  /* 16 waves of 64x64, 2 stages */
+    NNCONV_TILE_256x256_RING = 6, /* 4 waves of 128x128, ring of 4 32-element slices */
+    NNCONV_TILE_256x128_RING = 7, /* 4 waves of 128x64, ring of 3 */
+    NNCONV_TILE_256x64_RING = 8   /* 4 waves of 64x64, ring of 4 */
+} nnconv_tile;
+
+/* nnconv_fwd / nnconv_dgrad with the tile forced (an nnconv_tile value).
+ * Same arguments, semantics and errors, plus: INVALID_ARG for a negative
+ * tile; UNSUPPORTED when the tile is not one of nnconv_tile, or when the
+ * call would not run on the implicit-GEMM kernel (reduction channels per tap
+ * not a multiple of 64, depthwise or small-group convolution, the stem's
+ * 8-channel shape, operands not 16-byte aligned or past 2 GiB, backward-data
+ * with more than 4 stride phases). */
+nnconv_status nnconv_fwd_tile(const nnconv_desc *desc, const void *x, const void *w, void *y,
+                              float alpha, void *ws, size_t ws_bytes, void *hip_stream,
+                              int32_t tile);
+nnconv_status nnconv_dgrad_tile(const nnconv_desc *desc, const void *dy, const void *w, void *dx,
+                                float alpha, void *ws, size_t ws_bytes, void *hip_stream,
+                                int32_t tile);
+
 /* Backward-weight pass with the loss-scale step of Sec. 3.3 / Listing 6:
  *   dw = (accumulate ? dw : 0) + inv_loss_scale * sum_{n,p,q} dy * xz
  * The batch-pixel reduction is split over the workspace in fp32 and summed

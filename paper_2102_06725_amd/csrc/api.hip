@@ -408,8 +408,15 @@ TNPhase phase_of(int64_t m, int64_t mi, int64_t mj, int64_t oi_add, int64_t oj_a
     return f;
 }
 
+// Whether the 64-channel-slice kernel runs the forward / backward-data pass
+// of a shape that fast_shape() accepts (the tiles a caller may force).
+bool c64_fwd_shape(const Geom &G) { return !stem_shape(G) && G.cg % 64 == 0; }
+bool c64_dgrad_shape(const Geom &G) { return G.kg % 64 == 0 && G.sh * G.sw <= MAX_PHASES; }
+
+// tile: a C64Config to force on the 64-channel-slice kernel, or -1 for the
+// per-shape pick.
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
-                       hipStream_t st) {
+                       hipStream_t st, int tile = -1) {
     if (stem_shape(G)) {
         StemParams sp;
         sp.x = x;
@@ -472,8 +479,9 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     if (G.cg % 64 == 0) {
         p.nphase = 1;
         p.ph[0] = phase_of(p.M, p.mi, p.mj, 0, 0, 0, t);
-        return hip_status(launch_igemm_c64(G.dtype, pick_c64_geom(G, p.M, G.kg, (int64_t)t * G.cg), p,
-                                           G.ph > 0 || G.pw > 0, st));
+        const C64Config cfg =
+            tile >= 0 ? (C64Config)tile : pick_c64_geom(G, p.M, G.kg, (int64_t)t * G.cg);
+        return hip_status(launch_igemm_c64(G.dtype, cfg, p, G.ph > 0 || G.pw > 0, st));
     }
     return hip_status(launch_igemm_c8(G.dtype, pick_c8(G.kg), p, st));
 }
@@ -482,7 +490,7 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
 // output phase (h mod sigma_h, w mod sigma_w): within a phase every pixel
 // sees the same set of contributing taps.  wt is [g][R][S][Cg][Kg].
 nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx, float alpha,
-                         hipStream_t st) {
+                         hipStream_t st, int tile = -1) {
     TNParams base = tn_base();
     base.a = dy;
     base.a_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
@@ -524,7 +532,7 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
         p.taps.n += t;
         return t;
     };
-    if (G.kg % 64 == 0 && G.sh * G.sw <= MAX_PHASES) {
+    if (c64_dgrad_shape(G)) {
         // every stride phase in one launch; a phase without taps writes zeros
         TNParams p = base;
         p.taps.n = 0;
@@ -543,8 +551,8 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             }
         }
         if (p.nphase == 0) return NNCONV_OK;
-        return hip_status(
-            launch_igemm_c64(G.dtype, pick_c64_geom(G, rows, G.cg, max_red), p, pad, st));
+        const C64Config cfg = tile >= 0 ? (C64Config)tile : pick_c64_geom(G, rows, G.cg, max_red);
+        return hip_status(launch_igemm_c64(G.dtype, cfg, p, pad, st));
     }
     // Otherwise sigma_h * sigma_w launches, one per output phase (h mod
     // sigma_h, w mod sigma_w): within a phase every pixel sees the same set of
@@ -800,8 +808,16 @@ static nnconv_status check_ws(const Geom &G, nnconv_pass pass, const void *ws, s
     return NNCONV_OK;
 }
 
-NNCONV_API nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, const void *w, void *y,
-                                    float alpha, void *ws, size_t ws_bytes, void *hip_stream) {
+// Whether a forced tile can run this call: a tile of the 64-channel-slice
+// kernel other than the block-diagonal one, on a dense call that takes that
+// kernel with its operands as given.
+bool tile_ok(int tile) {
+    return tile >= C64_256x256 && tile <= C64R_256x64 && tile != C64D_128x64;
+}
+
+static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void *w, void *y,
+                              float alpha, void *ws, size_t ws_bytes, void *hip_stream,
+                              int tile) {
     Geom G;
     nnconv_status st = validate(desc, &G);
     if (st != NNCONV_OK) return st;
@@ -809,6 +825,12 @@ NNCONV_API nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, cons
     if (!aligned(x, 2) || !aligned(w, 2) || !aligned(y, 2)) return NNCONV_ERR_MISALIGNED;
     if ((st = check_ws(G, NNCONV_FWD, ws, ws_bytes)) != NNCONV_OK) return st;
     hipStream_t s = (hipStream_t)hip_stream;
+    if (tile >= 0) {
+        const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_fwd_shape(G) &&
+                           aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
+                           (G.layout == NNCONV_NHWC || aligned(ws, 16));
+        if (!tile_ok(tile) || !dense) return NNCONV_ERR_UNSUPPORTED;
+    }
     clear_stale_error();
     if (dw_shape(G)) {
         if (!aligned(x, 16) || !aligned(w, 2) || !aligned(y, 16) || !aligned(ws, 16))
@@ -821,19 +843,31 @@ NNCONV_API nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, cons
     const bool fast = fast_shape(G) && aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                       (G.layout == NNCONV_NHWC || aligned(ws, 16));
     if (!fast) return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
-    if (G.layout == NNCONV_NHWC) return fwd_fast(G, x, w, y, alpha, s);
+    if (G.layout == NNCONV_NHWC) return fwd_fast(G, x, w, y, alpha, s, tile);
     const Regions R = fast_regions(G, NNCONV_FWD);
     char *base = (char *)ws;
     void *xt = base + R.a, *wt = base + R.b, *yt = base + R.c;
     TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, s));
     TRY_HIP(launch_transpose16(w, wt, G.k, G.cg, G.r * G.s, G.cg, s));
-    if ((st = fwd_fast(G, xt, wt, yt, alpha, s)) != NNCONV_OK) return st;
+    if ((st = fwd_fast(G, xt, wt, yt, alpha, s, tile)) != NNCONV_OK) return st;
     return hip_status(launch_transpose16(yt, y, G.n, G.p * G.q, G.k, G.p * G.q, s));
 }
 
-NNCONV_API nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, const void *w,
-                                      void *dx, float alpha, void *ws, size_t ws_bytes,
-                                      void *hip_stream) {
+NNCONV_API nnconv_status nnconv_fwd(const nnconv_desc *desc, const void *x, const void *w, void *y,
+                                    float alpha, void *ws, size_t ws_bytes, void *hip_stream) {
+    return fwd_impl(desc, x, w, y, alpha, ws, ws_bytes, hip_stream, -1);
+}
+
+NNCONV_API nnconv_status nnconv_fwd_tile(const nnconv_desc *desc, const void *x, const void *w,
+                                         void *y, float alpha, void *ws, size_t ws_bytes,
+                                         void *hip_stream, int32_t tile) {
+    if (tile < 0) return NNCONV_ERR_INVALID_ARG;
+    return fwd_impl(desc, x, w, y, alpha, ws, ws_bytes, hip_stream, tile);
+}
+
+static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const void *w,
+                                void *dx, float alpha, void *ws, size_t ws_bytes,
+                                void *hip_stream, int tile) {
     Geom G;
     nnconv_status st = validate(desc, &G);
     if (st != NNCONV_OK) return st;
@@ -841,6 +875,12 @@ NNCONV_API nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, c
     if (!aligned(dy, 2) || !aligned(w, 2) || !aligned(dx, 2)) return NNCONV_ERR_MISALIGNED;
     if ((st = check_ws(G, NNCONV_DGRAD, ws, ws_bytes)) != NNCONV_OK) return st;
     hipStream_t s = (hipStream_t)hip_stream;
+    if (tile >= 0) {
+        const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_dgrad_shape(G) &&
+                           aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
+                           aligned(ws, 16);
+        if (!tile_ok(tile) || !dense) return NNCONV_ERR_UNSUPPORTED;
+    }
     clear_stale_error();
     if (dw_shape(G)) {
         if (!aligned(dy, 16) || !aligned(w, 2) || !aligned(dx, 16) || !aligned(ws, 16))
@@ -872,10 +912,23 @@ NNCONV_API nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, c
     }
     // [g][Kg][R*S*Cg] -> [g][R*S*Cg][Kg]
     TRY_HIP(launch_transpose16(wkrsc, wt, G.g, G.kg, G.r * G.s * G.cg, G.kg, s));
-    if ((st = dgrad_fast(G, dyn, wt, dxn, alpha, s)) != NNCONV_OK) return st;
+    if ((st = dgrad_fast(G, dyn, wt, dxn, alpha, s, tile)) != NNCONV_OK) return st;
     if (G.layout == NNCONV_NCHW)
         return hip_status(launch_transpose16(dxn, dx, G.n, G.h * G.w, G.c, G.h * G.w, s));
     return NNCONV_OK;
+}
+
+NNCONV_API nnconv_status nnconv_dgrad(const nnconv_desc *desc, const void *dy, const void *w,
+                                      void *dx, float alpha, void *ws, size_t ws_bytes,
+                                      void *hip_stream) {
+    return dgrad_impl(desc, dy, w, dx, alpha, ws, ws_bytes, hip_stream, -1);
+}
+
+NNCONV_API nnconv_status nnconv_dgrad_tile(const nnconv_desc *desc, const void *dy,
+                                           const void *w, void *dx, float alpha, void *ws,
+                                           size_t ws_bytes, void *hip_stream, int32_t tile) {
+    if (tile < 0) return NNCONV_ERR_INVALID_ARG;
+    return dgrad_impl(desc, dy, w, dx, alpha, ws, ws_bytes, hip_stream, tile);
 }
 
 NNCONV_API nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, const void *dy,

@@ -125,4 +125,58 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t nblocks) {
 // fall in different 16-byte bank groups.
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS staging and LDS hand-offs (shared by the matrix-core kernels)
+// ---------------------------------------------------------------------------
+
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Wait until at most `n` vector-memory operations of this wave are
+// outstanding.  Written as asm with a memory clobber so no load or store
+// moves across it.
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
+}
+
+// Workgroup barrier for LDS hand-offs between waves: first wait until this
+// wave's own LDS reads and writes have completed (s_barrier alone does not),
+// so data written before the barrier is what other waves read after it.  The
+// memory clobber also keeps the compiler from moving LDS accesses across it
+// (the direct-to-LDS loads are invisible to its dependence tracking).
+__device__ __forceinline__ void barrier_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Buffer descriptor (gfx9 format, raw addressing) for the bytes
+// [base + shift, base + bytes); empty when shift >= bytes.  The words are
+// made wave-uniform so they live in scalar registers.
+__device__ __forceinline__ i32x4 desc_at(const void *base, uint32_t bytes, uint32_t shift) {
+    const uint64_t a = (uint64_t)base + shift;
+    i32x4 d;
+    d[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)a);
+    d[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(a >> 32) & 0xFFFFu));
+    d[2] = __builtin_amdgcn_readfirstlane((int32_t)(shift < bytes ? bytes - shift : 0u));
+    d[3] = 0x00020000;
+    return d;
+}
+
+__device__ __forceinline__ i32x4 desc_of(const void *base, uint32_t bytes) {
+    return desc_at(base, bytes, 0);
+}
+
+// buffer_load_dwordx4 ... lds: lane i's 16 bytes from desc + voff go to LDS
+// byte address lds_addr + 16*i; offsets at or past the descriptor's range
+// deliver zeros.
+__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 desc) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(desc)
+        : "memory");
+}
+
 }  // namespace nnconv

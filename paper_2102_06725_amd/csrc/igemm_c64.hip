@@ -24,44 +24,6 @@ namespace nnconv {
 
 namespace c64 {
 
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-
-template <int n>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(n >= 0 && n < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
-}
-
-// Workgroup barrier for LDS hand-offs between waves: first wait until this
-// wave's own LDS reads and writes have completed (s_barrier alone does not),
-// so data written before the barrier is what other waves read after it.
-__device__ __forceinline__ void barrier_lds() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// Buffer descriptor for bytes [base + shift, base + bytes) (gfx9 format).
-__device__ __forceinline__ i32x4 desc_at(const void *base, uint32_t bytes, uint32_t shift) {
-    const uint64_t a = (uint64_t)base + shift;
-    i32x4 d;
-    d[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)a);
-    d[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(a >> 32) & 0xFFFFu));
-    d[2] = __builtin_amdgcn_readfirstlane((int32_t)(shift < bytes ? bytes - shift : 0u));
-    d[3] = 0x00020000;
-    return d;
-}
-
-// buffer_load_dwordx4 ... lds: lane i's 16 bytes go to LDS byte address
-// lds_addr + 16*i; offsets at or past the descriptor's range deliver zeros.
-__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 desc) {
-    asm volatile(
-        "s_mov_b32 m0, %0\n\t"
-        "buffer_load_dwordx4 %1, %2, 0 offen lds"
-        :
-        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(desc)
-        : "memory");
-}
-
 // LDS tile: BKC 16-byte chunks per row; row r, logical chunk c at slot
 // r*BKC + (c ^ swz(r)).  The 64 LDS banks serve a 16-byte read for 16 lanes
 // per cycle, and a fragment read has 16 consecutive rows at one logical
@@ -84,8 +46,16 @@ __device__ __forceinline__ int slot(int r, int c) {
 // super-groups, groups of at most 32 channels), so a wave's 32 output
 // columns meet only the matching 32 reduction channels of each 64-channel
 // slice: two of its four k-steps.
-template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool PAD, bool DIAG>
-__global__ __launch_bounds__(WM * WN * 64, (WM * WN == 4) ? ((BM * BN <= 128 * 128) ? 4 : 2) : 1)
+//
+// RING: the k-slices cycle through an LDS ring of STAGES buffers (STAGES - 1
+// slices in flight while one is multiplied), and each wave reads the
+// fragments of the next k-step -- across the slice boundary too -- before it
+// issues the matrix-core instructions of the current one, so LDS latency
+// overlaps MFMA work inside the wave instead of relying on other waves.
+// OCC: resident workgroups per CU the register budget is sized for.
+template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool PAD, bool DIAG,
+          bool RING, int OCC>
+__global__ __launch_bounds__(WM * WN * 64, OCC)
 void igemm_c64_kernel(const TNParams P) {
     using namespace c64;
     constexpr int NW = WM * WN;             // waves per workgroup
@@ -106,7 +76,7 @@ void igemm_c64_kernel(const TNParams P) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WM, wn = wave / WM;
 
     // phase of this workgroup: phases own consecutive ranges of hardware
@@ -177,34 +147,56 @@ void igemm_c64_kernel(const TNParams P) {
 
     int ld_t = 0, ld_c = 0;  // tap and channel base of the next slice to load
 
-    auto issue = [&](int buf) {
-        const int t = tap0 + ld_t;
+    // Per-tap byte shifts, tap t held by lane t: the loop reads them back
+    // with v_readlane instead of loading the tap table from memory each slice.
+    const int tl = tap0 + (lane < ntaps ? lane : 0);
+    const uint32_t tap_ashift =
+        (uint32_t)(P.taps.dh[tl] * P.a_w + P.taps.dw[tl]) * (uint32_t)P.a_c * 2u;
+    const uint32_t tap_boff = (uint32_t)P.taps.boff[tl] * 2u;
+
+    // One slice's staging, split so that its loads can be spread between
+    // matrix-core instructions: prepare() sets the slice's descriptors and
+    // shifts (wave-uniform) and advances to the next slice, load(j) issues load
+    // j (the A loads, then the B loads).  A slice past the end of the
+    // reduction (live = false) gets empty descriptors: its loads deliver
+    // zeros without touching memory.
+    uint32_t sl_ashift = 0, sl_sb = 0;
+    int sl_t = 0;
+    i32x4 sl_da = {}, sl_db = {};
+    auto prepare = [&](int buf, bool live) {
         // A: x / dy rows; the tap's pixel shift can be negative, so it is
         // added to the lane offsets; the channel base moves the descriptor
-        const uint32_t ashift =
-            (uint32_t)(P.taps.dh[t] * P.a_w + P.taps.dw[t]) * (uint32_t)P.a_c * 2u;
-        const i32x4 da = desc_at(P.a, P.a_bytes, (uint32_t)ld_c * 2u);
-        const i32x4 db = desc_at(P.b, P.b_bytes, (uint32_t)(P.taps.boff[t] + ld_c) * 2u);
-        const uint32_t sb = lds0 + (uint32_t)(buf * STAGE_SLOTS) * 16u;
-#pragma unroll
-        for (int j = 0; j < A_LD; ++j) {
-            uint32_t off = a_voff[j] + ashift;
-            if constexpr (PAD) {
-                if (!((a_mask[j] >> ld_t) & 1)) off = OOB_OFFSET;
-            } else {
-                if (a_voff[j] == OOB_OFFSET) off = OOB_OFFSET;
-            }
-            dma16(sb + (uint32_t)((wave * A_LD + j) * 64) * 16u, off, da);
-        }
-#pragma unroll
-        for (int j = 0; j < B_LD; ++j)
-            dma16(sb + (uint32_t)(A_SLOTS + (wave * B_LD + j) * 64) * 16u, b_voff[j], db);
+        sl_ashift = (uint32_t)__builtin_amdgcn_readlane((int)tap_ashift, ld_t);
+        const uint32_t bshift = (uint32_t)__builtin_amdgcn_readlane((int)tap_boff, ld_t);
+        sl_da = desc_at(P.a, live ? P.a_bytes : 0u, (uint32_t)ld_c * 2u);
+        sl_db = desc_at(P.b, live ? P.b_bytes : 0u, bshift + (uint32_t)ld_c * 2u);
+        sl_sb = lds0 + (uint32_t)(buf * STAGE_SLOTS) * 16u;
+        sl_t = ld_t;
         // taps inner, channel slices outer: the taps of one channel slice
         // re-read overlapping pixels back to back, while they are still in L2
         if (++ld_t == ntaps) {
             ld_t = 0;
             ld_c += BK;
         }
+    };
+    auto load = [&](int j) {
+        if (j < A_LD) {
+            uint32_t off = a_voff[j] + sl_ashift;
+            if constexpr (PAD) {
+                if (!((a_mask[j] >> sl_t) & 1)) off = OOB_OFFSET;
+            } else {
+                if (a_voff[j] == OOB_OFFSET) off = OOB_OFFSET;
+            }
+            dma16(sl_sb + (uint32_t)((wave * A_LD + j) * 64) * 16u, off, sl_da);
+        } else {
+            const int jb = j - A_LD;
+            dma16(sl_sb + (uint32_t)(A_SLOTS + (wave * B_LD + jb) * 64) * 16u, b_voff[jb], sl_db);
+        }
+    };
+    auto issue = [&](int buf) {
+        prepare(buf, true);
+#pragma unroll
+        for (int j = 0; j < LOADS; ++j) load(j);
     };
 
     f32x16 acc[FN][FM];
@@ -260,6 +252,85 @@ void igemm_c64_kernel(const TNParams P) {
             wait_vmcnt<0>();
             barrier_lds();
             compute(&lds[0]);
+        }
+    } else if constexpr (RING) {
+        static_assert(!DIAG && STAGES >= 2 && BKC % 4 == 0, "ring: dense, 2+ stages, even k-steps");
+        constexpr int KS = BKC / 2;  // 16-deep k-steps per slice (even)
+        u32x4 fa[2][FM], fb[2][FN];
+        auto read_frags = [&](const u32x4 *st, int ks, u32x4 (&a)[FM], u32x4 (&b)[FN]) {
+            const int kc = 2 * ks + khalf;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) a[i] = st[slot<BKC>(wm * WTM + i * 32 + l32, kc)];
+#pragma unroll
+            for (int j = 0; j < FN; ++j) b[j] = st[A_SLOTS + slot<BKC>(wn * WTN + j * 32 + l32, kc)];
+        };
+        auto mma = [&](const u32x4 (&a)[FM], const u32x4 (&b)[FN]) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int i = 0; i < FM; ++i) acc[j][i] = mfma32<T>(b[j], a[i], acc[j][i]);
+        };
+        // the same k-step with the loads of a prepared slice placed between
+        // its matrix-core instructions (the scheduling fences keep them
+        // there), so issuing them costs no matrix-core time
+        auto mma_loads = [&](const u32x4 (&a)[FM], const u32x4 (&b)[FN]) {
+            constexpr int NM = FM * FN;
+            constexpr int STRIDE = NM >= 2 * LOADS ? NM / LOADS : 1;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    const int m = j * FM + i;
+                    acc[j][i] = mfma32<T>(b[j], a[i], acc[j][i]);
+                    if (m % STRIDE == 0 && m / STRIDE < LOADS) {
+                        __builtin_amdgcn_sched_barrier(0);
+                        load(m / STRIDE);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            }
+#pragma unroll
+            for (int l = (NM + STRIDE - 1) / STRIDE; l < LOADS; ++l) load(l);
+        };
+        // the k-steps of one slice but its last: each reads the next k-step's
+        // fragments, then multiplies
+        auto slice_body = [&](const u32x4 *st) {
+#pragma unroll
+            for (int ks = 0; ks + 1 < KS; ++ks) {
+                read_frags(st, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+                mma(fa[ks & 1], fb[ks & 1]);
+            }
+        };
+        if (k_iters > 0) {
+            // prologue: every buffer of the ring gets a slice (slices past
+            // the end load nothing, but keep the wait counts uniform)
+            for (int s = 0; s < STAGES; ++s) {
+                prepare(s, s < k_iters);
+#pragma unroll
+                for (int j = 0; j < LOADS; ++j) load(j);
+            }
+            wait_vmcnt<(STAGES - 1) * LOADS>();  // slice 0 landed
+            barrier_lds();
+            read_frags(&lds[0], 0, fa[0], fb[0]);
+            for (int kt = 0; kt + 1 < k_iters; ++kt) {
+                slice_body(&lds[(kt % STAGES) * STAGE_SLOTS]);
+                // slice kt + 1 has landed once at most STAGES - 2 later
+                // slices are pending; after the barrier no wave reads slice
+                // kt any more (its last fragments are in registers), so its
+                // buffer takes slice kt + STAGES.  The fence keeps the
+                // k-steps above ahead of the wait.
+                __builtin_amdgcn_sched_barrier(0);
+                wait_vmcnt<(STAGES - 2) * LOADS>();
+                barrier_lds();
+                read_frags(&lds[((kt + 1) % STAGES) * STAGE_SLOTS], 0, fa[0], fb[0]);
+                prepare(kt % STAGES, kt + STAGES < k_iters);
+                mma_loads(fa[1], fb[1]);
+            }
+            slice_body(&lds[((k_iters - 1) % STAGES) * STAGE_SLOTS]);
+            mma(fa[1], fb[1]);
+            // slices past the end may still be landing (as zeros) in the
+            // buffers the epilogue reuses
+            wait_vmcnt<0>();
         }
     } else if (k_iters > 0) {
         const int pro = k_iters < STAGES - 1 ? k_iters : STAGES - 1;
@@ -329,7 +400,9 @@ void igemm_c64_kernel(const TNParams P) {
     }
 }
 
-template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool DIAG = false>
+template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool DIAG = false,
+          bool RING = false,
+          int OCC = (WM * WN == 4) ? ((BM * BN <= 128 * 128) ? 4 : 2) : 1>
 static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
     p.tiles_n = (p.ncols + BN - 1) / BN;
     int64_t nb = 0;
@@ -341,10 +414,10 @@ static hipError_t launch_c64_cfg(TNParams &p, bool pad, hipStream_t st) {
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (pad)
-        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, true, DIAG>),
+        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, true, DIAG, RING, OCC>),
                            dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     else
-        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, false, DIAG>),
+        hipLaunchKernelGGL((igemm_c64_kernel<T, BM, BN, WM, WN, BKC, STAGES, false, DIAG, RING, OCC>),
                            dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
@@ -367,6 +440,9 @@ static hipError_t launch_c64_t(C64Config cfg, TNParams &p, bool pad, hipStream_t
         case C64_128x128: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 2>(p, pad, st);
         case C64S_128x64: return launch_c64_cfg<T, 128, 64, 2, 2, 8, 1>(p, pad, st);
         case C64D_128x64: return launch_c64_cfg<T, 128, 64, 2, 2, 8, 1, true>(p, pad, st);
+        case C64R_256x256: return launch_c64_cfg<T, 256, 256, 2, 2, 4, 4, false, true, 1>(p, pad, st);
+        case C64R_256x128: return launch_c64_cfg<T, 256, 128, 2, 2, 4, 3, false, true, 2>(p, pad, st);
+        case C64R_256x64: return launch_c64_cfg<T, 256, 64, 4, 1, 4, 4, false, true, 2>(p, pad, st);
         case C64S_128x128:
         default: return launch_c64_cfg<T, 128, 128, 2, 2, 8, 1>(p, pad, st);
     }

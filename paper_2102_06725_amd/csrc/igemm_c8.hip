@@ -21,49 +21,6 @@
 
 namespace nnconv {
 
-// Wait until at most `n` vector-memory operations of this wave are
-// outstanding.  Written as asm with a memory clobber so no load or store
-// moves across it.
-template <int n>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(n >= 0 && n < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
-}
-
-// Workgroup barrier for LDS hand-offs between waves: first wait until this
-// wave's own LDS reads and writes have completed (s_barrier alone does not),
-// so data written before the barrier is what other waves read after it.  The
-// memory clobber also keeps the compiler from moving LDS accesses across it
-// (the direct-to-LDS loads are invisible to its dependence tracking).
-__device__ __forceinline__ void barrier_lds() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Buffer descriptor words for a raw byte range (gfx9 format).
-__device__ __forceinline__ i32x4 make_desc(const void *base, uint32_t bytes) {
-    const uint64_t a = (uint64_t)base;
-    i32x4 d;
-    d[0] = (int32_t)(uint32_t)a;
-    d[1] = (int32_t)((uint32_t)(a >> 32) & 0xFFFFu);
-    d[2] = (int32_t)bytes;
-    d[3] = 0x00020000;
-    return d;
-}
-
-// buffer_load_dwordx4 ... lds: lane i's 16 bytes from desc+voff go to LDS
-// byte address lds_addr + 16*i.  Out-of-range offsets deliver zeros.
-__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 desc) {
-    asm volatile(
-        "s_mov_b32 m0, %0\n\t"
-        "buffer_load_dwordx4 %1, %2, 0 offen lds"
-        :
-        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(desc)
-        : "memory");
-}
-
 // 64 LDS banks serve 16 lanes of a 16-byte read per cycle: the 16 rows of a
 // fragment read must land in 16 distinct 16-byte bank groups of 256 bytes.
 // 128-byte rows (BKC 8): parity of r picks the half, (r>>1)&7 the chunk;
@@ -108,8 +65,8 @@ __global__ __launch_bounds__(256, 2) void igemm_c8_kernel(const TNParams P) {
     const int tn = rem - tm * P.tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    const i32x4 ra = make_desc(P.a, P.a_bytes);
-    const i32x4 rb = make_desc(P.b, P.b_bytes);
+    const i32x4 ra = desc_of(P.a, P.a_bytes);
+    const i32x4 rb = desc_of(P.b, P.b_bytes);
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void *)&lds[0];
 
     // Load instruction j of this wave fills slots [(wave*LD + j)*64, +64); lane

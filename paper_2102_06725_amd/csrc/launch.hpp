@@ -88,8 +88,13 @@ enum C64Config { C64_256x256 = 0,   // 8 waves, 64-element slices, 2 stages
                  C64S_128x128 = 2,  // single stage (several workgroups per CU)
                  C64S_128x64 = 3,
                  C64W_256x256 = 4,    // 16 waves of 64x64, 2 stages
-                 C64D_128x64 = 5 };   // C64S_128x64 for block-diagonal 64x64 weights
+                 C64D_128x64 = 5,     // C64S_128x64 for block-diagonal 64x64 weights
                                       // (32x32 blocks): half the k-steps per wave
+                 // LDS ring of 32-element slices with register-prefetched
+                 // fragments (one wave per SIMD for 256x256: 128x128 per wave)
+                 C64R_256x256 = 6,    // 4 waves of 128x128, 4 stages (128 KB)
+                 C64R_256x128 = 7,    // 4 waves of 128x64, 3 stages (72 KB), 2 per CU
+                 C64R_256x64 = 8 };   // 4 waves of 64x64, 4 stages (80 KB), 2 per CU
 hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hipStream_t st);
 
 // Forward pass for 8-channel (16-byte) channel-last pixels, 64 output

@@ -23,9 +23,6 @@ namespace nnconv {
 
 namespace stem {
 
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-
 constexpr int TH = 16, TW = 16;  // output tile
 constexpr int K = 64;            // output channels
 // Waves per workgroup (one workgroup per CU): two per SIMD, so one wave's
@@ -37,39 +34,6 @@ constexpr int WG_WAVES = 8;
 static_assert(8 % FWD_WAVES == 0, "forward: whole 32-pixel fragments per wave");
 static_assert((TH * TW * 8) % (64 * FWD_WAVES) == 0, "forward: whole store rounds");
 static_assert((TH * TW * K / 8) % (64 * WG_WAVES) == 0, "backward-weight: whole dy loads");
-
-template <int n>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(n >= 0 && n < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
-}
-
-// Barrier for LDS hand-offs between waves: the wave's own LDS accesses are
-// complete before it signals (s_barrier alone does not wait for them).
-__device__ __forceinline__ void barrier_lds() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-__device__ __forceinline__ i32x4 desc_of(const void *base, uint32_t bytes) {
-    const uint64_t a = (uint64_t)base;
-    i32x4 d;
-    d[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)a);
-    d[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(a >> 32) & 0xFFFFu));
-    d[2] = __builtin_amdgcn_readfirstlane((int32_t)bytes);
-    d[3] = 0x00020000;
-    return d;
-}
-
-// buffer_load_dwordx4 ... lds: lane i's 16 bytes land at lds_addr + 16*i;
-// offsets past the descriptor's range deliver zeros.
-__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 desc) {
-    asm volatile(
-        "s_mov_b32 m0, %0\n\t"
-        "buffer_load_dwordx4 %1, %2, 0 offen lds"
-        :
-        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(desc)
-        : "memory");
-}
 
 template <int R, int S, int SH, int SW>
 struct Geo {

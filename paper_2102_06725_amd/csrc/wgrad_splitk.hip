@@ -21,42 +21,8 @@ namespace nnconv {
 
 namespace wgs {
 
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-
-template <int n>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(n >= 0 && n < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
-}
-
-// Workgroup barrier for LDS hand-offs between waves: first wait until this
-// wave's own LDS reads and writes have completed (s_barrier alone does not),
-// so data written before the barrier is what other waves read after it.
-__device__ __forceinline__ void barrier_lds() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-__device__ __forceinline__ i32x4 desc_of(const void *base, uint32_t bytes) {
-    const uint64_t a = (uint64_t)base;
-    i32x4 d;
-    d[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)a);
-    d[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(a >> 32) & 0xFFFFu));
-    d[2] = __builtin_amdgcn_readfirstlane((int32_t)bytes);
-    d[3] = 0x00020000;
-    return d;
-}
-
-__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 desc) {
-    asm volatile(
-        "s_mov_b32 m0, %0\n\t"
-        "buffer_load_dwordx4 %1, %2, 0 offen lds"
-        :
-        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(desc)
-        : "memory");
-}
 
 // Row p of a tile with ROWB-byte rows: logical 64-byte segment s lives at
 // physical segment s ^ swz(p).  A transposing read touches rows p0..p0+3

@@ -32,9 +32,22 @@ NNCONV_F32 = 2
 NNCONV_FWD = 0
 NNCONV_DGRAD = 1
 NNCONV_WGRAD = 2
+# nnconv_tile: tiles of the implicit-GEMM forward / backward-data kernel
+NNCONV_TILE_256x256_8W = 0
+NNCONV_TILE_128x128_2S = 1
+NNCONV_TILE_128x128 = 2
+NNCONV_TILE_128x64 = 3
+NNCONV_TILE_256x256_16W = 4
+NNCONV_TILE_256x256_RING = 6
+NNCONV_TILE_256x128_RING = 7
+NNCONV_TILE_256x64_RING = 8
+TILES = (NNCONV_TILE_256x256_8W, NNCONV_TILE_128x128_2S, NNCONV_TILE_128x128, NNCONV_TILE_128x64,
+         NNCONV_TILE_256x256_16W, NNCONV_TILE_256x256_RING, NNCONV_TILE_256x128_RING,
+         NNCONV_TILE_256x64_RING)
 
 EXPORTS = ("nnconv_version", "nnconv_last_hip_error", "nnconv_status_string", "nnconv_output_dims",
-           "nnconv_workspace_size", "nnconv_fwd", "nnconv_dgrad", "nnconv_wgrad",
+           "nnconv_workspace_size", "nnconv_fwd", "nnconv_dgrad", "nnconv_fwd_tile",
+           "nnconv_dgrad_tile", "nnconv_wgrad",
            "nnconv_nchw_to_nhwc", "nnconv_nhwc_to_nchw", "nnconv_pad_channels",
            "nnconv_weight_kcrs_to_krsc", "nnconv_weight_krsc_to_kcrs",
            "nnconv_loss_scaler_init", "nnconv_loss_scaler_update", "nnconv_sgd_update")
@@ -97,6 +110,10 @@ def load(path: str | None = None):
     lib.nnconv_workspace_size.argtypes = [_DESCP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
     lib.nnconv_fwd.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP, ctypes.c_size_t, _VP]
     lib.nnconv_dgrad.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP, ctypes.c_size_t, _VP]
+    lib.nnconv_fwd_tile.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP, ctypes.c_size_t,
+                                    _VP, _I32]
+    lib.nnconv_dgrad_tile.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP,
+                                      ctypes.c_size_t, _VP, _I32]
     lib.nnconv_wgrad.argtypes = [_DESCP, _VP, _VP, _VP, _I32, ctypes.c_float, _I32, _VP, _VP,
                                  ctypes.c_size_t, _VP]
     lib.nnconv_nchw_to_nhwc.argtypes = [_VP, _VP, _I32, _I32, _I32, _I32, _I32, _VP]
@@ -159,6 +176,16 @@ def nnconv_fwd(desc, x, w, y, alpha, ws, ws_bytes, stream) -> int:
 
 def nnconv_dgrad(desc, dy, w, dx, alpha, ws, ws_bytes, stream) -> int:
     return load().nnconv_dgrad(ctypes.byref(desc), dy, w, dx, float(alpha), ws, ws_bytes, stream)
+
+
+def nnconv_fwd_tile(desc, x, w, y, alpha, ws, ws_bytes, stream, tile) -> int:
+    return load().nnconv_fwd_tile(ctypes.byref(desc), x, w, y, float(alpha), ws, ws_bytes, stream,
+                                  int(tile))
+
+
+def nnconv_dgrad_tile(desc, dy, w, dx, alpha, ws, ws_bytes, stream, tile) -> int:
+    return load().nnconv_dgrad_tile(ctypes.byref(desc), dy, w, dx, float(alpha), ws, ws_bytes,
+                                    stream, int(tile))
 
 
 def nnconv_wgrad(desc, x, dy, dw, dw_dtype, inv_loss_scale, accumulate, overflow_flag, ws,

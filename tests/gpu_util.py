@@ -144,10 +144,12 @@ def stream():
 
 
 def run_gpu(case: Case, t, passes=("fwd", "dgrad", "wgrad"), dw_dtype=None, inv_scale=None,
-            accumulate=0, dw_old=None, flag=None, dw_shift=0, in_shift=0, out_shift=0):
+            accumulate=0, dw_old=None, flag=None, dw_shift=0, in_shift=0, out_shift=0,
+            tile=None):
     """Run the requested passes on the GPU; returns dict of output bits /
     fp32 values in the case's layout.  in_shift / out_shift move x, w, dy /
-    y, dx that many 16-bit elements off 16-byte alignment."""
+    y, dx that many 16-bit elements off 16-byte alignment.  tile: force this
+    implicit-GEMM tile on the forward and backward-data passes."""
     L = case.layer
     tt = torch()
     d = case.desc()
@@ -161,14 +163,24 @@ def run_gpu(case: Case, t, passes=("fwd", "dgrad", "wgrad"), dw_dtype=None, inv_
     if "fwd" in passes:
         y = Guarded(L.n * L.k * L.p * L.q, shift=out_shift)
         ws, nb = workspace(d, nc.NNCONV_FWD)
-        nc.check(nc.nnconv_fwd(d, x.data_ptr(), w.data_ptr(), y.ptr(), case.alpha, ws.data_ptr(),
-                               nb, s), "fwd")
+        if tile is None:
+            st = nc.nnconv_fwd(d, x.data_ptr(), w.data_ptr(), y.ptr(), case.alpha, ws.data_ptr(),
+                               nb, s)
+        else:
+            st = nc.nnconv_fwd_tile(d, x.data_ptr(), w.data_ptr(), y.ptr(), case.alpha,
+                                    ws.data_ptr(), nb, s, tile)
+        nc.check(st, "fwd")
         out["y"] = y
     if "dgrad" in passes:
         dx = Guarded(L.n * L.c * L.h * L.w, shift=out_shift)
         ws, nb = workspace(d, nc.NNCONV_DGRAD)
-        nc.check(nc.nnconv_dgrad(d, dy.data_ptr(), w.data_ptr(), dx.ptr(), case.alpha,
-                                 ws.data_ptr(), nb, s), "dgrad")
+        if tile is None:
+            st = nc.nnconv_dgrad(d, dy.data_ptr(), w.data_ptr(), dx.ptr(), case.alpha,
+                                 ws.data_ptr(), nb, s)
+        else:
+            st = nc.nnconv_dgrad_tile(d, dy.data_ptr(), w.data_ptr(), dx.ptr(), case.alpha,
+                                      ws.data_ptr(), nb, s, tile)
+        nc.check(st, "dgrad")
         out["dx"] = dx
     if "wgrad" in passes:
         fp32 = dw_dtype in (None, nc.NNCONV_F32)
@@ -211,10 +223,10 @@ def to_nchw(case: Case, which: str, a):
     return a
 
 
-def full_parity(case: Case, passes=("fwd", "dgrad", "wgrad")):
+def full_parity(case: Case, passes=("fwd", "dgrad", "wgrad"), tile=None):
     """Run every pass, compare against the full oracle.  Returns errors."""
     t = case.tensors()
-    got = run_gpu(case, t, passes)
+    got = run_gpu(case, t, passes, tile=tile)
     x, w, dy = nchw_f64(case, t)
     cv = oracle_conv(case)
     L = case.layer

@@ -173,3 +173,34 @@ def test_sgd_update_validation(nnlib):
     # count 0 is a no-op that touches nothing, w16 NULL ignores w16_dtype
     assert call(count=0) == nc.NNCONV_OK
     assert call(count=0, w16=None, w16_dtype=7, state=None, flag=None) == nc.NNCONV_OK
+
+
+def test_forced_tile_validation(nnlib):
+    """The _tile variants refuse, before anything is queued, a negative tile,
+    a value that is not a dense implicit-GEMM tile, and calls that would not
+    run on that kernel."""
+    inv, uns = nc.NNCONV_ERR_INVALID_ARG, nc.NNCONV_ERR_UNSUPPORTED
+    dense = nc.make_desc(2, 64, 8, 8, 64, 3, 3, pad=(1, 1))
+    calls = (nc.nnconv_fwd_tile, nc.nnconv_dgrad_tile)
+    for f in calls:
+        assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, -1) == inv
+        for bad in (5, 9, 99):  # block-diagonal tile, out of range
+            assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, bad) == uns
+        # 16 reduction channels per tap: not the 64-channel-slice kernel
+        small = nc.make_desc(2, 16, 8, 8, 16, 3, 3, pad=(1, 1))
+        assert f(small, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns
+        # depthwise and small groups have kernels of their own
+        dwc = nc.make_desc(2, 64, 8, 8, 64, 3, 3, pad=(1, 1), groups=64)
+        assert f(dwc, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns
+        grp = nc.make_desc(2, 64, 8, 8, 64, 3, 3, pad=(1, 1), groups=16)
+        assert f(grp, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns
+        # operands off 16-byte alignment take the direct kernels
+        assert f(dense, FAKE + 2, FAKE + 2, FAKE + 2, 1.0, FAKE, 1 << 30, None, 2) == uns
+        # still the ordinary checks first
+        assert f(dense, None, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == inv
+    # the stem's 8-channel shape has its own forward kernel
+    stem = nc.make_desc(2, 8, 32, 32, 64, 7, 7, stride=(2, 2), pad=(3, 3))
+    assert nc.nnconv_fwd_tile(stem, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns
+    # backward-data with more than four stride phases
+    s3 = nc.make_desc(2, 64, 9, 9, 64, 3, 3, stride=(3, 3), pad=(1, 1))
+    assert nc.nnconv_dgrad_tile(s3, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns

@@ -378,7 +378,11 @@ C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
     if (ncols == 256 && red >= 1024 && m > 98 * 256 && m <= 256 * 256) return C64W_256x256;
     const int64_t big_tiles = ((m + 255) / 256) * ((ncols + 255) / 256);
     if (ncols >= 256 && red >= BIG_RED && big_tiles >= MIN_BIG_TILES) return C64_256x256;
-    return red >= LONG_RED ? C64_128x128 : C64S_128x128;
+    // fewer 128x128 tiles than one round of single-stage workgroups (four
+    // per CU): the pipelined tile already pays from half the long reduction
+    const int64_t tiles = ((m + 127) / 128) * ((ncols + 127) / 128);
+    const int64_t long_red = tiles < 4 * 256 ? LONG_RED / 2 : LONG_RED;
+    return red >= long_red ? C64_128x128 : C64S_128x128;
 }
 
 // Compute units of the current device (the persistent kernels launch one
@@ -537,7 +541,9 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
         TNParams p = base;
         p.taps.n = 0;
         p.nphase = 0;
-        int64_t rows = 0, max_red = 0;
+        // the tile is picked for the row-weighted mean reduction of the
+        // phases (a stride-2 3x3 dgrad has 1, 2, 2 and 4 taps per phase)
+        int64_t rows = 0, red_rows = 0;
         for (int64_t phh = 0; phh < G.sh; ++phh) {
             for (int64_t phw = 0; phw < G.sw; ++phw) {
                 const int64_t mi = phh < G.h ? (G.h - phh + G.sh - 1) / G.sh : 0;
@@ -547,11 +553,12 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
                 const int cnt = add_phase_taps(p, phh, phw);
                 p.ph[p.nphase++] = phase_of(G.n * mi * mj, mi, mj, phh, phw, start, cnt);
                 rows += G.n * mi * mj;
-                if (cnt * G.kg > max_red) max_red = cnt * G.kg;
+                red_rows += G.n * mi * mj * cnt * G.kg;
             }
         }
         if (p.nphase == 0) return NNCONV_OK;
-        const C64Config cfg = tile >= 0 ? (C64Config)tile : pick_c64_geom(G, rows, G.cg, max_red);
+        const C64Config cfg =
+            tile >= 0 ? (C64Config)tile : pick_c64_geom(G, rows, G.cg, red_rows / rows);
         return hip_status(launch_igemm_c64(G.dtype, cfg, p, pad, st));
     }
     // Otherwise sigma_h * sigma_w launches, one per output phase (h mod

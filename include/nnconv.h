@@ -32,8 +32,10 @@
  *     void*; NULL means the default stream).  Calls return once queued.
  *     They queue kernel launches only (no memset, copy or event), so a
  *     sequence of calls may be captured into a HIP graph and replayed.
- *   - The library keeps no mutable global state: calls are reentrant, and
- *     calls on different streams with disjoint buffers may run concurrently.
+ *   - The library keeps no mutable global state (the one exception is the
+ *     scratch array of nnconv_wgrad_noalloc, see there): calls are
+ *     reentrant, and calls on different streams with disjoint buffers may
+ *     run concurrently.
  *   - Fast (matrix-core) paths need 16-byte aligned pointers and Cg, Kg that
  *     are multiples of 8; other valid shapes run on slower direct kernels
  *     with identical semantics.
@@ -179,6 +181,30 @@ nnconv_status nnconv_dgrad_tile(const nnconv_desc *desc, const void *dy, const v
 nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, const void *dy, void *dw,
                            int32_t dw_dtype, float inv_loss_scale, int32_t accumulate,
                            int32_t *overflow_flag, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* For callers that cannot allocate device memory or size a workspace --
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc: nnconv_wgrad with the workspace taken from a library-owned
+ * scratch array of NNCONV_NOALLOC_WS_BYTES (64 MiB) instead of an argument.
+ * Same arguments (minus ws, ws_bytes), semantics, results (bitwise equal to
+ * nnconv_wgrad's) and errors, plus NNCONV_ERR_WORKSPACE, returned before
+ * anything is queued, when the geometry needs more workspace than the
+ * scratch holds (nnconv_workspace_size(desc, NNCONV_WGRAD) >
+ * NNCONV_NOALLOC_WS_BYTES; every channel-last ResNet-50 layer at batch 256
+ * fits).
+ *   - The scratch is a device array of the library: every GPU the library
+ *     runs on holds one copy from the first call on it (made with that GPU
+ *     current, outside graph capture) until the process ends.  The call
+ *     itself allocates nothing.
+ *   - Every call on one GPU shares that GPU's copy, which keeps the last
+ *     call's contents; nothing in it needs to start at zero.  Calls that
+ *     overlap on one GPU (several streams or threads without ordering)
+ *     race on it: order them on one stream. */
+#define NNCONV_NOALLOC_WS_BYTES (64 * 1024 * 1024)
+nnconv_status nnconv_wgrad_noalloc(const nnconv_desc *desc, const void *x, const void *dy,
+                                   void *dw, int32_t dw_dtype, float inv_loss_scale,
+                                   int32_t accumulate, int32_t *overflow_flag,
+                                   void *hip_stream);
 
 /* Layout transforms (pure data movement of 16-bit elements, bit exact).
  *

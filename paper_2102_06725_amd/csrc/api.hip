@@ -4,6 +4,8 @@
 
 #include <string.h>
 
+#include <mutex>
+
 #include "launch.hpp"
 
 #define NNCONV_API extern "C" __attribute__((visibility("default")))
@@ -938,22 +940,29 @@ NNCONV_API nnconv_status nnconv_dgrad_tile(const nnconv_desc *desc, const void *
     return dgrad_impl(desc, dy, w, dx, alpha, ws, ws_bytes, hip_stream, tile);
 }
 
-NNCONV_API nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, const void *dy,
-                                      void *dw, int32_t dw_dtype, float inv_loss_scale,
-                                      int32_t accumulate, int32_t *overflow_flag, void *ws,
-                                      size_t ws_bytes, void *hip_stream) {
-    Geom G;
-    nnconv_status st = validate(desc, &G);
+// Argument checks of the backward-weight pass that need no workspace.
+static nnconv_status wgrad_check(const nnconv_desc *desc, const void *x, const void *dy,
+                                 const void *dw, int32_t dw_dtype, int32_t accumulate,
+                                 const int32_t *overflow_flag, Geom *G) {
+    nnconv_status st = validate(desc, G);
     if (st != NNCONV_OK) return st;
     if (!x || !dy || !dw) return NNCONV_ERR_INVALID_ARG;
     if (dw_dtype != NNCONV_F32 && dw_dtype != NNCONV_F16 && dw_dtype != NNCONV_BF16)
         return NNCONV_ERR_INVALID_ARG;
-    if (dw_dtype != NNCONV_F32 && dw_dtype != G.dtype) return NNCONV_ERR_UNSUPPORTED;
+    if (dw_dtype != NNCONV_F32 && dw_dtype != G->dtype) return NNCONV_ERR_UNSUPPORTED;
     if (accumulate != 0 && accumulate != 1) return NNCONV_ERR_INVALID_ARG;
     if (!aligned(x, 2) || !aligned(dy, 2) || !aligned(dw, dw_dtype == NNCONV_F32 ? 4 : 2) ||
         (overflow_flag && !aligned(overflow_flag, 4)))
         return NNCONV_ERR_MISALIGNED;
-    if ((st = check_ws(G, NNCONV_WGRAD, ws, ws_bytes)) != NNCONV_OK) return st;
+    return NNCONV_OK;
+}
+
+// The backward-weight pass on a checked geometry with a workspace of at
+// least workspace_bytes(G, NNCONV_WGRAD) bytes.
+static nnconv_status wgrad_run(const Geom &G, const void *x, const void *dy, void *dw,
+                               int32_t dw_dtype, float inv_loss_scale, int32_t accumulate,
+                               int32_t *overflow_flag, void *ws, void *hip_stream) {
+    nnconv_status st;
     hipStream_t s = (hipStream_t)hip_stream;
     clear_stale_error();
     const int out_code = dw_dtype == NNCONV_F32 ? 2 : (dw_dtype == NNCONV_F16 ? 0 : 1);
@@ -991,6 +1000,70 @@ NNCONV_API nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, co
     return hip_status(launch_wgrad_reduce(part, pl.splits, count, dw, out_code, inv_loss_scale,
                                           accumulate, overflow_flag, kcrs, (int32_t)G.cg,
                                           (int32_t)(G.r * G.s), s));
+}
+
+NNCONV_API nnconv_status nnconv_wgrad(const nnconv_desc *desc, const void *x, const void *dy,
+                                      void *dw, int32_t dw_dtype, float inv_loss_scale,
+                                      int32_t accumulate, int32_t *overflow_flag, void *ws,
+                                      size_t ws_bytes, void *hip_stream) {
+    Geom G;
+    nnconv_status st = wgrad_check(desc, x, dy, dw, dw_dtype, accumulate, overflow_flag, &G);
+    if (st != NNCONV_OK) return st;
+    if ((st = check_ws(G, NNCONV_WGRAD, ws, ws_bytes)) != NNCONV_OK) return st;
+    return wgrad_run(G, x, dy, dw, dw_dtype, inv_loss_scale, accumulate, overflow_flag, ws,
+                     hip_stream);
+}
+
+// ---------------------------------------------------------------------------
+// backward-weight without a caller workspace
+// ---------------------------------------------------------------------------
+
+// Library-owned scratch of the allocation-free entry point: a file-scope
+// device array, so each GPU the library runs on holds one copy (its
+// NNCONV_NOALLOC_WS_BYTES stay allocated until the process ends).  The
+// array's name is a host-side stand-in: host code uses only the device
+// address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[NNCONV_NOALLOC_WS_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::once_flag scratch_once[MAX_DEVICES];
+void *scratch_ptr[MAX_DEVICES];
+hipError_t scratch_err[MAX_DEVICES];
+
+// Device address of the current device's scratch copy, looked up once per
+// device (with that device current) and kept.
+hipError_t device_scratch(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::call_once(scratch_once[dev], [dev] {
+        void *p = nullptr;
+        scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        scratch_ptr[dev] = p;
+    });
+    if (scratch_err[dev] != hipSuccess) return scratch_err[dev];
+    if (!scratch_ptr[dev]) return hipErrorInvalidSymbol;
+    *out = scratch_ptr[dev];
+    return hipSuccess;
+}
+}  // namespace
+
+NNCONV_API nnconv_status nnconv_wgrad_noalloc(const nnconv_desc *desc, const void *x,
+                                              const void *dy, void *dw, int32_t dw_dtype,
+                                              float inv_loss_scale, int32_t accumulate,
+                                              int32_t *overflow_flag, void *hip_stream) {
+    Geom G;
+    nnconv_status st = wgrad_check(desc, x, dy, dw, dw_dtype, accumulate, overflow_flag, &G);
+    if (st != NNCONV_OK) return st;
+    if (workspace_bytes(G, NNCONV_WGRAD) > (size_t)NNCONV_NOALLOC_WS_BYTES)
+        return NNCONV_ERR_WORKSPACE;
+    void *ws = nullptr;
+    const hipError_t e = device_scratch(&ws);
+    if (e != hipSuccess) return hip_status(e);
+    return wgrad_run(G, x, dy, dw, dw_dtype, inv_loss_scale, accumulate, overflow_flag, ws,
+                     hip_stream);
 }
 
 // ---------------------------------------------------------------------------

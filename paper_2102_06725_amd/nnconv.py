@@ -32,6 +32,7 @@ NNCONV_F32 = 2
 NNCONV_FWD = 0
 NNCONV_DGRAD = 1
 NNCONV_WGRAD = 2
+NNCONV_NOALLOC_WS_BYTES = 64 * 1024 * 1024
 # nnconv_tile: tiles of the implicit-GEMM forward / backward-data kernel
 NNCONV_TILE_256x256_8W = 0
 NNCONV_TILE_128x128_2S = 1
@@ -47,7 +48,7 @@ TILES = (NNCONV_TILE_256x256_8W, NNCONV_TILE_128x128_2S, NNCONV_TILE_128x128, NN
 
 EXPORTS = ("nnconv_version", "nnconv_last_hip_error", "nnconv_status_string", "nnconv_output_dims",
            "nnconv_workspace_size", "nnconv_fwd", "nnconv_dgrad", "nnconv_fwd_tile",
-           "nnconv_dgrad_tile", "nnconv_wgrad",
+           "nnconv_dgrad_tile", "nnconv_wgrad", "nnconv_wgrad_noalloc",
            "nnconv_nchw_to_nhwc", "nnconv_nhwc_to_nchw", "nnconv_pad_channels",
            "nnconv_weight_kcrs_to_krsc", "nnconv_weight_krsc_to_kcrs",
            "nnconv_loss_scaler_init", "nnconv_loss_scaler_update", "nnconv_sgd_update")
@@ -110,6 +111,8 @@ def load(path: str | None = None):
     lib.nnconv_workspace_size.argtypes = [_DESCP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
     lib.nnconv_fwd.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP, ctypes.c_size_t, _VP]
     lib.nnconv_dgrad.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP, ctypes.c_size_t, _VP]
+    lib.nnconv_wgrad_noalloc.argtypes = [_DESCP, _VP, _VP, _VP, _I32, ctypes.c_float, _I32,
+                                         _VP, _VP]
     lib.nnconv_fwd_tile.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP, ctypes.c_size_t,
                                     _VP, _I32]
     lib.nnconv_dgrad_tile.argtypes = [_DESCP, _VP, _VP, _VP, ctypes.c_float, _VP,
@@ -193,6 +196,13 @@ def nnconv_wgrad(desc, x, dy, dw, dw_dtype, inv_loss_scale, accumulate, overflow
     return load().nnconv_wgrad(ctypes.byref(desc), x, dy, dw, int(dw_dtype),
                                float(inv_loss_scale), int(accumulate), overflow_flag, ws,
                                ws_bytes, stream)
+
+
+def nnconv_wgrad_noalloc(desc, x, dy, dw, dw_dtype, inv_loss_scale, accumulate, overflow_flag,
+                         stream) -> int:
+    return load().nnconv_wgrad_noalloc(ctypes.byref(desc), x, dy, dw, int(dw_dtype),
+                                       float(inv_loss_scale), int(accumulate), overflow_flag,
+                                       stream)
 
 
 def nnconv_nchw_to_nhwc(src, dst, n, c, h, w, c_pad, stream) -> int:

@@ -204,3 +204,24 @@ def test_forced_tile_validation(nnlib):
     # backward-data with more than four stride phases
     s3 = nc.make_desc(2, 64, 9, 9, 64, 3, 3, stride=(3, 3), pad=(1, 1))
     assert nc.nnconv_dgrad_tile(s3, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns
+
+
+def test_noalloc_wgrad_validation(nnlib):
+    """nnconv_wgrad_noalloc refuses, before anything is queued, what
+    nnconv_wgrad refuses, and geometries whose workspace exceeds its scratch."""
+    inv, mis = nc.NNCONV_ERR_INVALID_ARG, nc.NNCONV_ERR_MISALIGNED
+    d = good_desc()
+    call = nc.nnconv_wgrad_noalloc
+    assert call(d, None, FAKE, FAKE, nc.NNCONV_F32, 1.0, 0, None, None) == inv
+    assert call(d, FAKE, FAKE, FAKE, 5, 1.0, 0, None, None) == inv
+    assert call(d, FAKE, FAKE, FAKE, nc.NNCONV_F32, 1.0, 2, None, None) == inv
+    assert call(d, FAKE, FAKE, FAKE + 2, nc.NNCONV_F32, 1.0, 0, None, None) == mis
+    assert call(d, FAKE, FAKE, FAKE, nc.NNCONV_F32, 1.0, 0, FAKE + 1, None) == mis
+    assert call(d, FAKE, FAKE, FAKE, nc.NNCONV_BF16, 1.0, 0, None, None) == nc.NNCONV_ERR_UNSUPPORTED
+    assert call(good_desc(n=0), FAKE, FAKE, FAKE, nc.NNCONV_F32, 1.0, 0, None, None) == inv
+    # NCHW copies of a 56x56x256 batch-64 activation exceed the 64 MiB scratch
+    big = nc.make_desc(64, 256, 56, 56, 64, 1, 1, layout=nc.NNCONV_NCHW)
+    st, need = nc.nnconv_workspace_size(big, nc.NNCONV_WGRAD)
+    assert st == nc.NNCONV_OK and need > nc.NNCONV_NOALLOC_WS_BYTES
+    assert call(big, FAKE, FAKE, FAKE, nc.NNCONV_F32, 1.0, 0, None, None) == \
+        nc.NNCONV_ERR_WORKSPACE

@@ -13,9 +13,13 @@ inputs are seeded synthetic draws already resident in HBM.  Prints one
 JSON line.
 
 value = sum of algorithmic FLOPs (2*N*K*P*Q*Cg*R*S per pass, stem with its
-3 logical channels) / wall time of the timed steps.  The timed steps carry
-no markers; per-pass times and the forward launch durations come from the
-same number of steps run again afterwards with HIP events around every pass.
+3 logical channels) / time of the timed steps, cold: before every timed step
+a 1 GiB scratch buffer is written (outside the timed region), so no operand
+starts in the 256 MB last-level cache.  The same K steps back to back (warm)
+are reported beside it.  The GPU clock is sampled during the timed steps.
+The timed steps carry no markers; per-pass, per-layer and per-launch figures
+come from the same number of steps run again afterwards with HIP events
+around every pass.
 """
 from __future__ import annotations
 
@@ -37,6 +41,7 @@ METRIC_DW = ("depthwise conv fwd+dgrad+wgrad compulsory HBM GB/s on EfficientNet
              "% of 8 TB/s")
 METRIC_RNXT = ("grouped conv fwd+dgrad+wgrad algorithmic TFLOP/s on ResNeXt-50 32x4d shapes; "
                "% of fp16 MFMA peak")
+METRIC_LAT = "conv fwd+dgrad+wgrad latency of one 3x3 16->16 NCHW convolution at batch 2; us"
 
 
 def parse():
@@ -45,15 +50,20 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="sweep",
-                    choices=["sweep", "cfg2", "cfg3", "cfg4", "effdw", "rnxt"],
-                    help="sweep: the 53 ResNet-50 layers (the headline metric); effdw: the 16 "
-                         "depthwise layers of EfficientNet-B0 at batch 128 (one channel per "
-                         "group, reported as HBM GB/s); rnxt: the 16 grouped 3x3 layers of "
-                         "ResNeXt-50 32x4d at batch 128 (algorithmic TFLOP/s)")
+                    choices=["sweep", "cfg1", "cfg2", "cfg3", "cfg4", "effdw", "rnxt"],
+                    help="sweep: the 53 ResNet-50 layers at batch 256 (the headline metric); "
+                         "cfg1: one 3x3 16->16 NCHW convolution at batch 2 (latency, us per "
+                         "step); cfg2: the stage-1 bottleneck at batch 64; cfg3: the stage "
+                         "transitions at batch 128; cfg4: the stem at batch 128 (fwd + wgrad); "
+                         "effdw: the 16 depthwise layers of EfficientNet-B0 at batch 128 (one "
+                         "channel per group, reported as HBM GB/s); rnxt: the 16 grouped 3x3 "
+                         "layers of ResNeXt-50 32x4d at batch 128 (algorithmic TFLOP/s)")
     ap.add_argument("--dtype", default="f16", choices=["f16", "bf16"])
     ap.add_argument("--batch", type=int, default=0, help="override the batch size")
     ap.add_argument("--cpu-seconds", type=float, default=30.0,
                     help="upper bound on the oracle CPU-baseline sample (0 disables it)")
+    ap.add_argument("--flush-mib", type=int, default=1024,
+                    help="scratch written before every cold timed step (0: warm only)")
     ap.add_argument("--no-events", action="store_true",
                     help="skip the event-instrumented steps (per-pass times, roofline)")
     ap.add_argument("--layers", default="",
@@ -86,7 +96,7 @@ def layers_for(args):
             keep = set(args.layers.split(","))
             expanded = [l for l in expanded if l.name in keep]
         return wl, expanded
-    cfg = {"cfg2": 2, "cfg3": 3, "cfg4": 4}[args.workload]
+    cfg = {"cfg1": 1, "cfg2": 2, "cfg3": 3, "cfg4": 4}[args.workload]
     wl = I.workload(cfg, args.dtype, batch=args.batch or None)
     return wl, list(wl.layers)
 
@@ -121,7 +131,8 @@ class LayerBuffers:
         self.dx = torch.empty((L.n, L.h, L.w, L.c), device=dev, dtype=tdt) if L.dgrad else None
         self.dw = torch.empty((L.k, L.r, L.s, cg), device=dev, dtype=torch.float32)
         self.desc = nc.make_desc(L.n, L.c, L.h, L.w, L.k, L.r, L.s, (L.stride, L.stride),
-                                 (L.pad, L.pad), (L.dil, L.dil), L.groups, nc.NNCONV_NHWC,
+                                 (L.pad, L.pad), (L.dil, L.dil), L.groups,
+                                 nc.NNCONV_NCHW if wl.layout == "nchw" else nc.NNCONV_NHWC,
                                  nc.NNCONV_F16 if wl.dtype == "f16" else nc.NNCONV_BF16)
         self.ws_need = {}
         for p in (nc.NNCONV_FWD, nc.NNCONV_DGRAD, nc.NNCONV_WGRAD):
@@ -191,10 +202,11 @@ def fwd_source_hash():
     return h.hexdigest()
 
 
-def stored_traffic():
-    """HBM bytes per forward launch from the committed FETCH_SIZE /
-    WRITE_SIZE counter summary, or None when it is missing or was taken on
-    other kernel sources."""
+def stored_traffic(kind="mfma"):
+    """HBM bytes per forward launch of the MFMA-bound (kind "mfma") or
+    HBM-bound ("hbm") sweep layers from the committed FETCH_SIZE / WRITE_SIZE
+    counter summary, or None when it is missing or was taken on other kernel
+    sources."""
     try:
         kv = {}
         with open(TRAFFIC_FILE) as f:
@@ -204,7 +216,8 @@ def stored_traffic():
                     kv[k.strip()] = v.strip()
         if kv.get("source_sha256") != fwd_source_hash():
             return None
-        return float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"])
+        return float(kv["%s_fetch_bytes_per_launch" % kind]) + \
+            float(kv["%s_write_bytes_per_launch" % kind])
     except (OSError, KeyError, ValueError):
         return None
 
@@ -227,14 +240,30 @@ def is_forward_launch(names, i):
 
 def summarize_profile(args):
     """Prints per-kernel totals and the forward-launch figures from rocprofv3
-    CSV output (kernel trace; FETCH_SIZE and WRITE_SIZE counter runs) of
-    `bench.py --calib-copy-mib M --steps K --warmup W`."""
+    CSV output of `bench.py --calib-copy-mib M --steps K --warmup W`: a
+    kernel trace, FETCH_SIZE and WRITE_SIZE counter runs (bytes per forward
+    launch, for the MFMA-bound and the HBM-bound layers of the workload), and
+    any other counter run (per-kernel averages per dispatch, with the MFMA
+    utilisation and LDS bank-conflict rate derived where their counters are
+    present)."""
     import csv
     import glob
     import collections
-    nl = len(layers_for(args)[1])
+    layers = layers_for(args)[1]
+    nl = len(layers)
     skip = args.warmup * nl
+    mf, hb = fwd_sets(layers)
+    sets = (("mfma", set(mf)), ("hbm", set(hb)))
     out = []
+
+    def fwd_launches(names):
+        """Forward launches after the warm-up steps, with their layer index."""
+        f = [i for i in range(len(names)) if is_forward_launch(names, i)][skip:]
+        return [(i, j % nl) for j, i in enumerate(f)]
+
+    def family(n):
+        return n.split("(")[0].replace("void ", "") if "nnconv::" in n else "(torch / runtime)"
+
     for path in sorted(glob.glob(os.path.join(args.summarize_profile, "**", "*kernel_trace.csv"),
                                  recursive=True)):
         rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
@@ -242,44 +271,90 @@ def summarize_profile(args):
         dur = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows]
         fam = collections.defaultdict(lambda: [0, 0])
         for n, d in zip(names, dur):
-            key = n.split("(")[0].replace("void ", "") if "nnconv::" in n else "(torch / runtime)"
-            fam[key][0] += 1
-            fam[key][1] += d
+            fam[family(n)][0] += 1
+            fam[family(n)][1] += d
         tot = sum(v[1] for v in fam.values())
         out.append("kernel trace: %s" % os.path.relpath(path, args.summarize_profile))
         out.append("%-72s %7s %12s %10s %6s" % ("kernel", "calls", "total_us", "avg_us", "%"))
         for k, v in sorted(fam.items(), key=lambda kv: -kv[1][1]):
             out.append("%-72s %7d %12.1f %10.2f %6.2f" % (k[:72], v[0], v[1] / 1e3,
                                                           v[1] / v[0] / 1e3, 100.0 * v[1] / tot))
-        fwd = [i for i in range(len(names)) if is_forward_launch(names, i)][skip:]
+        fwd = fwd_launches(names)
         out.append("forward launches (after %d warm-up ones): %d, average %.2f us, total %.1f us"
-                   % (skip, len(fwd), sum(dur[i] for i in fwd) / max(1, len(fwd)) / 1e3,
-                      sum(dur[i] for i in fwd) / 1e3))
-    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
-        for path in sorted(glob.glob(os.path.join(args.summarize_profile, "**",
-                                                  "*counter_collection.csv"), recursive=True)):
-            rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
-            if not rows:
-                continue
-            rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+                   % (skip, len(fwd), sum(dur[i] for i, _ in fwd) / max(1, len(fwd)) / 1e3,
+                      sum(dur[i] for i, _ in fwd) / 1e3))
+        for kind, members in sets:
+            sel = [i for i, li in fwd if li in members]
+            if sel:
+                out.append("forward launches of the %s-bound layers: %d, average %.2f us"
+                           % (kind, len(sel), sum(dur[i] for i in sel) / len(sel) / 1e3))
+    for path in sorted(glob.glob(os.path.join(args.summarize_profile, "**",
+                                              "*counter_collection.csv"), recursive=True)):
+        allrows = list(csv.DictReader(open(path)))
+        counters = sorted({r["Counter_Name"] for r in allrows})
+        for counter in counters:
+            rows = sorted((r for r in allrows if r["Counter_Name"] == counter),
+                          key=lambda r: int(r["Dispatch_Id"]))
             names = [r["Kernel_Name"] for r in rows]
-            kib = [float(r["Counter_Value"]) for r in rows]
+            vals = [float(r["Counter_Value"]) for r in rows]
+            if counter not in ("FETCH_SIZE", "WRITE_SIZE"):
+                continue
             line = "%s (%s):" % (counter, os.path.relpath(path, args.summarize_profile))
             factor = None
             if args.calib_copy_mib:
                 copy = [i for i, n in enumerate(names) if "pad_channels" in n][0]
-                factor = args.calib_copy_mib * 1024.0 / kib[copy]
+                factor = args.calib_copy_mib * 1024.0 / vals[copy]
                 line += " copy of %d MiB reads as %.1f KiB (factor %.4f);" % (
-                    args.calib_copy_mib, kib[copy], factor)
-            fwd = [i for i in range(len(names)) if is_forward_launch(names, i)][skip:]
-            per = sum(kib[i] for i in fwd) / max(1, len(fwd)) * 1024.0
-            line += " forward launches %d, %.1f MB per launch as counted" % (len(fwd), per / 1e6)
-            if factor is not None:
-                line += ", %.1f MB scaled" % (per * factor / 1e6)
+                    args.calib_copy_mib, vals[copy], factor)
+            fwd = fwd_launches(names)
             out.append(line)
-            if factor is not None:
-                out.append("%s_bytes_per_launch: %.0f" % (
-                    "fetch" if counter == "FETCH_SIZE" else "write", per * factor))
+            for kind, members in sets:
+                sel = [i for i, li in fwd if li in members]
+                if not sel:
+                    continue
+                per = sum(vals[i] for i in sel) / len(sel) * 1024.0
+                out.append("  forward launches of the %s-bound layers: %d, %.1f MB per launch as "
+                           "counted%s" % (kind, len(sel), per / 1e6, "" if factor is None else
+                                          ", %.1f MB scaled" % (per * factor / 1e6)))
+                if factor is not None:
+                    out.append("%s_%s_bytes_per_launch: %.0f" % (
+                        kind, "fetch" if counter == "FETCH_SIZE" else "write", per * factor))
+        others = [c for c in counters if c not in ("FETCH_SIZE", "WRITE_SIZE")]
+        if not others:
+            continue
+        # per dispatch: counter values and duration; then averages per kernel
+        disp = collections.defaultdict(dict)
+        for r in allrows:
+            d = disp[int(r["Dispatch_Id"])]
+            d["name"] = r["Kernel_Name"]
+            d["dur"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            d[r["Counter_Name"]] = float(r["Counter_Value"])
+        fam = collections.OrderedDict()
+        for k in sorted(disp):
+            if "nnconv::" in disp[k]["name"]:
+                fam.setdefault(family(disp[k]["name"]), []).append(disp[k])
+        out.append("counters per dispatch (%s), averaged per kernel:"
+                   % os.path.relpath(path, args.summarize_profile))
+        for name, ds in fam.items():
+            avg = {c: sum(d.get(c, 0.0) for d in ds) / len(ds) for c in others}
+            dur = sum(d["dur"] for d in ds) / len(ds)
+            out.append("%s  n=%d  avg %.2f us" % (name[:100], len(ds), dur / 1e3))
+            out.append("    " + "  ".join("%s=%.4g" % kv for kv in sorted(avg.items())))
+            ga = avg.get("GRBM_GUI_ACTIVE")
+            if ga:
+                # GRBM_GUI_ACTIVE sums the cycles of the 8 XCDs
+                out.append("    clock %.3f GHz (GRBM_GUI_ACTIVE / 8 / duration)" % (ga / 8 / dur))
+                if "SQ_VALU_MFMA_BUSY_CYCLES" in avg:
+                    out.append("    MFMA utilisation %.3f (SQ_VALU_MFMA_BUSY_CYCLES / (1024 "
+                               "SIMDs x GRBM_GUI_ACTIVE / 8))"
+                               % (avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (1024 * ga / 8)))
+            if avg.get("SQ_LDS_IDX_ACTIVE"):
+                if "SQ_LDS_BANK_CONFLICT" in avg:
+                    out.append("    LDS bank-conflict cycles / LDS active cycles %.4f"
+                               % (avg["SQ_LDS_BANK_CONFLICT"] / avg["SQ_LDS_IDX_ACTIVE"]))
+            if avg.get("TCC_HIT_sum") is not None and "TCC_MISS_sum" in avg:
+                h, m = avg["TCC_HIT_sum"], avg["TCC_MISS_sum"]
+                out.append("    L2 hit rate %.3f" % (h / max(1.0, h + m)))
     out.append("source_sha256: %s" % fwd_source_hash())
     print("\n".join(out))
 
@@ -343,10 +418,13 @@ def cpu_baseline(args, wl):
 UPDATE_BYTES_PER_PARAM = 22  # read master, momentum, grad (fp32); write master, momentum, w16
 
 
-def measure_update(args, layers, torch, nc, dev, sptr, stream, reps=20):
+def measure_update(args, layers, torch, nc, dev, sptr, stream, flush, reps=20):
     """Times the fused fp32 master-weight update (momentum SGD, loss-scale
     division, 16-bit copy) over every weight of the workload's layers held in
-    one flat buffer -- outside the convolution metric, reported beside it."""
+    one flat buffer -- outside the convolution metric, reported beside it.
+    Cold: each launch follows a scratch write that evicts its operands from
+    the last-level cache (back-to-back launches would find the 516 MB of
+    operands partly cached); the warm back-to-back figure is reported too."""
     count = sum(L.k * (L.c_alg // L.groups) * L.r * L.s for L in layers)
     count = (count + 3) // 4 * 4
     g = torch.Generator(device="cpu").manual_seed(5)
@@ -373,12 +451,91 @@ def measure_update(args, layers, torch, nc, dev, sptr, stream, reps=20):
         call()
     e1.record(stream)
     torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) * 1e3 / reps
+    warm_us = e0.elapsed_time(e1) * 1e3 / reps
+    us = warm_us
+    if flush is not None:
+        tot = 0.0
+        for k in range(reps):
+            flush.fill_(k & 0xFF)
+            e0.record(stream)
+            call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            tot += e0.elapsed_time(e1) * 1e3
+        us = tot / reps
     gbps = count * UPDATE_BYTES_PER_PARAM / (us * 1e-6) / 1e9
     return {"kernel": "sgd_update_kernel (one launch over all %d conv weights)" % count,
             "params": count, "us_per_launch": us, "bound": "hbm",
             "achieved": gbps, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": gbps / PEAK_HBM_GBS}
+            "frac": gbps / PEAK_HBM_GBS, "cache": "cold" if flush is not None else "warm",
+            "warm_us_per_launch": warm_us,
+            "warm_achieved": count * UPDATE_BYTES_PER_PARAM / (warm_us * 1e-6) / 1e9}
+
+
+class ClockSampler:
+    """Samples the GPU shader clock (the current level of the card's
+    pp_dpm_sclk in sysfs, else amd-smi) on a host thread while armed; only
+    samples taken inside armed intervals count."""
+
+    def __init__(self, period_s=0.002):
+        import glob
+        import threading
+        self.period = period_s
+        paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = paths[0] if paths else None
+        self.source = "sysfs pp_dpm_sclk" if self.path else "amd-smi metric -c"
+        self.samples = []
+        self.armed = False
+        self.stop = False
+        self.t = threading.Thread(target=self._run, daemon=True)
+        self.t.start()
+
+    def _read(self):
+        import re
+        import subprocess
+        try:
+            if self.path:
+                with open(self.path) as f:
+                    for line in f:
+                        if line.rstrip().endswith("*"):
+                            m = re.search(r"(\d+)\s*[Mm]hz", line)
+                            return float(m.group(1)) if m else None
+                return None
+            out = subprocess.run(["amd-smi", "metric", "-c", "--json"], capture_output=True,
+                                 text=True, timeout=5).stdout
+            vals = [float(v) for v in re.findall(r'"clk":\s*\{\s*"value":\s*(\d+)', out)]
+            return sum(vals) / len(vals) if vals else None
+        except Exception:
+            return None
+
+    def _run(self):
+        while not self.stop:
+            if self.armed:
+                v = self._read()
+                if v is not None and self.armed:
+                    self.samples.append(v)
+            time.sleep(self.period if self.path else 0.05)
+
+    def close(self):
+        self.stop = True
+        self.t.join(timeout=2)
+
+    def summary(self):
+        busy = [v for v in self.samples if v >= 500.0]  # deep-sleep readings excluded
+        if not busy:
+            return None
+        mean = sum(busy) / len(busy)
+        return {"source": self.source, "samples": len(busy), "mean_mhz": mean,
+                "min_mhz": min(busy), "max_mhz": max(busy),
+                "peak_tflops_at_mean": 256 * 4096 * mean * 1e6 / 1e12}
+
+
+def fwd_sets(layers):
+    """Indices of the layers whose forward pass is MFMA-bound / HBM-bound by
+    the compulsory-byte roofline."""
+    mf = [i for i, L in enumerate(layers) if roofline_us(L, "fwd")[1] == "mfma"]
+    hb = [i for i, L in enumerate(layers) if roofline_us(L, "fwd")[1] == "hbm"]
+    return mf, hb
 
 
 def main():
@@ -406,6 +563,8 @@ def main():
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     flag = torch.zeros(1, dtype=torch.int32, device=dev)
     inv_s = 1.0 / wl.loss_scale
+    flush = (torch.empty(args.flush_mib * 1024 * 1024, dtype=torch.uint8, device=dev)
+             if args.flush_mib > 0 else None)
     if args.calib_copy_mib:
         rows = args.calib_copy_mib * 1024 * 1024 // COPY_ROW_BYTES
         src = torch.ones((rows, COPY_ROW_BYTES // 2), device=dev, dtype=torch.float16)
@@ -444,20 +603,40 @@ def main():
         one_step(None)
     torch.cuda.synchronize()
 
-    # The timed steps carry no markers: an event record between every two
-    # launches costs about 0.7 ms per step of the ResNet-50 sweep.
+    clock = ClockSampler()
+    # Warm: the K steps back to back (the last-level cache keeps what the
+    # previous step left in it).  The timed steps carry no markers: an event
+    # record between every two launches costs about 0.7 ms per sweep step.
     torch.cuda.synchronize()
+    clock.armed = True
     t0 = time.perf_counter()
     for _ in range(args.steps):
         one_step(None)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    elapsed = t1 - t0
+    warm_s = time.perf_counter() - t0
+    clock.armed = False
+    # Cold (the headline): every timed step starts after a scratch write of
+    # flush_mib MiB, which leaves no operand in the 256 MB last-level cache;
+    # the writes and their synchronisation are outside the timed region.
+    cold_s = None
+    if flush is not None:
+        cold_s = 0.0
+        for k in range(args.steps):
+            flush.fill_(k & 0xFF)
+            torch.cuda.synchronize()
+            clock.armed = True
+            t0 = time.perf_counter()
+            one_step(None)
+            torch.cuda.synchronize()
+            cold_s += time.perf_counter() - t0
+            clock.armed = False
+    clock.close()
+    elapsed = cold_s if cold_s is not None else warm_s
     if int(flag.item()) != 0:
         print("warning: overflow flag set during the benchmark", file=sys.stderr)
 
-    # Per-pass and per-launch figures: the same number of steps again, with
-    # HIP events around every pass (not part of `value`).
+    # Per-pass, per-layer and per-launch figures: the same number of steps
+    # again, warm, with HIP events around every pass (not part of `value`).
     use_ev = not args.no_events
     ev_steps = []
     if use_ev:
@@ -468,63 +647,79 @@ def main():
         torch.cuda.synchronize()
 
     step_flops = sum(L.flops() * (3 if L.dgrad else 2) for L in layers)
-    value = step_flops * args.steps / elapsed / 1e12
     depthwise = args.workload == "effdw"
+    latency = args.workload == "cfg1"
     step_bytes = sum(compulsory_bytes(L, p) for L in layers
                      for p in (("fwd", "dgrad", "wgrad") if L.dgrad else ("fwd", "wgrad")))
-    if depthwise:  # bound by HBM: report the compulsory bytes moved per second
-        value = step_bytes * args.steps / elapsed / 1e9
 
-    # per-pass time from the event-instrumented steps
-    pass_ms = {"fwd": 0.0, "dgrad": 0.0, "wgrad": 0.0}
-    pass_flops = {"fwd": 0, "dgrad": 0, "wgrad": 0}
-    pass_launch_units = {"fwd": 0, "dgrad": 0, "wgrad": 0}
-    if use_ev:
-        for ev in ev_steps:
-            for i, b in enumerate(bufs):
-                pass_ms["fwd"] += ev[i][0].elapsed_time(ev[i][1])
-                pass_ms["dgrad"] += ev[i][1].elapsed_time(ev[i][2])
-                pass_ms["wgrad"] += ev[i][2].elapsed_time(ev[i][3])
-        for L in layers:
-            pass_flops["fwd"] += L.flops() * args.steps
-            pass_launch_units["fwd"] += args.steps
-            pass_flops["wgrad"] += L.flops() * args.steps
-            pass_launch_units["wgrad"] += args.steps
-            if L.dgrad:
-                pass_flops["dgrad"] += L.flops() * args.steps
-                pass_launch_units["dgrad"] += args.steps
-    roofline = None
-    per_pass = {}
-    if use_ev:
-        for k in pass_ms:
-            if pass_ms[k] > 0:
-                per_pass[k] = {"ms_per_step": pass_ms[k] / args.steps,
-                               "tflops": pass_flops[k] / (pass_ms[k] * 1e-3) / 1e12}
-        # The forward pass is one kernel launch per layer (the implicit-GEMM
-        # forward kernel), so its per-call event time is that kernel's launch
-        # duration.
-        fwd_avg_ms = pass_ms["fwd"] / pass_launch_units["fwd"]
-        fwd_avg_flops = pass_flops["fwd"] / pass_launch_units["fwd"]
-        ach = fwd_avg_flops / (fwd_avg_ms * 1e-3) / 1e12
-        traffic = stored_traffic() if args.workload == "sweep" and not args.layers and \
-            not args.batch and args.dtype == "f16" else None
-        roofline = {"kernel": "forward implicit GEMM (igemm_c64_kernel; stem_fwd_kernel for "
-                              "the stem), one launch per nnconv_fwd call",
-                    "bound": "mfma", "achieved": ach, "peak": PEAK_F16_TFLOPS,
-                    "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS, "traffic": traffic,
-                    "avg_launch_us": fwd_avg_ms * 1e3,
-                    "avg_flops_per_launch": fwd_avg_flops}
-        if depthwise:
-            fwd_bytes = sum(compulsory_bytes(L, "fwd") for L in layers) / len(layers)
-            gbs = fwd_bytes / (fwd_avg_ms * 1e-3) / 1e9
-            roofline = {"kernel": "depthwise forward (dwt_fwd_kernel), one launch per "
-                                  "nnconv_fwd call",
-                        "bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": gbs / PEAK_HBM_GBS, "traffic": None,
-                        "avg_launch_us": fwd_avg_ms * 1e3,
-                        "avg_bytes_per_launch": fwd_bytes}
+    def rate(seconds):
+        if latency:     # microseconds per step
+            return seconds / args.steps * 1e6
+        if depthwise:   # bound by HBM: compulsory bytes moved per second
+            return step_bytes * args.steps / seconds / 1e9
+        return step_flops * args.steps / seconds / 1e12
 
-    update = measure_update(args, layers, torch, nc, dev, sptr, stream) if use_ev else None
+    value = rate(elapsed)
+
+    per_pass, roofline, roofline_hbm, attainable = {}, None, None, None
+    if use_ev:
+        # event time of layer i, pass index pi, averaged over the steps (ms)
+        def ev_ms(i, pi):
+            return sum(ev[i][pi].elapsed_time(ev[i][pi + 1]) for ev in ev_steps) / args.steps
+
+        for pi, pname in enumerate(("fwd", "dgrad", "wgrad")):
+            ls = [i for i, L in enumerate(layers) if pname != "dgrad" or L.dgrad]
+            ms = sum(ev_ms(i, pi) for i in ls)
+            if ms > 0:
+                per_pass[pname] = {"ms_per_step": ms,
+                                   "tflops": sum(layers[i].flops() for i in ls) / ms / 1e9}
+        # compulsory-byte roofline over every layer-pass of the step
+        roof_ms = meas_ms = 0.0
+        for i, L in enumerate(layers):
+            for pi, pname in enumerate(("fwd", "dgrad", "wgrad")):
+                if pname == "dgrad" and not L.dgrad:
+                    continue
+                roof_ms += roofline_us(L, pname)[0] / 1e3
+                meas_ms += ev_ms(i, pi)
+        attainable = {"roofline_ms_per_step": roof_ms, "measured_ms_per_step": meas_ms,
+                      "frac": roof_ms / meas_ms,
+                      "note": "sum over every layer-pass of max(executed flop / MFMA peak, "
+                              "compulsory bytes / HBM peak) over the sum of their event times"}
+        # The forward pass is one kernel launch per call, so its event time is
+        # that launch's duration.  MFMA-bound and HBM-bound layers (by the
+        # compulsory-byte roofline) are reported against their own peaks.
+        mf, hb = fwd_sets(layers)
+        if mf:
+            ms = sum(ev_ms(i, 0) for i in mf) / len(mf)
+            fl = sum(layers[i].flops() for i in mf) / len(mf)
+            ach = fl / (ms * 1e-3) / 1e12
+            traffic = stored_traffic("mfma") if args.workload == "sweep" and not args.layers \
+                and not args.batch and args.dtype == "f16" else None
+            roofline = {"kernel": "forward implicit GEMM (igemm_c64_kernel), the %d layers of "
+                                  "the workload whose forward pass is MFMA-bound" % len(mf),
+                        "bound": "mfma", "achieved": ach, "peak": PEAK_F16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": ach / PEAK_F16_TFLOPS, "traffic": traffic,
+                        "avg_launch_us": ms * 1e3, "avg_flops_per_launch": fl,
+                        "frac_of_attainable": sum(roofline_us(layers[i], "fwd")[0] for i in mf)
+                        / 1e3 / len(mf) / ms}
+        if hb:
+            ms = sum(ev_ms(i, 0) for i in hb) / len(hb)
+            by = sum(compulsory_bytes(layers[i], "fwd") for i in hb) / len(hb)
+            gbs = by / (ms * 1e-3) / 1e9
+            traffic = stored_traffic("hbm") if args.workload == "sweep" and not args.layers \
+                and not args.batch and args.dtype == "f16" else None
+            kern = "depthwise forward (dwt_fwd_kernel)" if depthwise else \
+                "forward implicit GEMM (igemm_c64_kernel; stem_fwd_kernel for the stem)"
+            roofline_hbm = {"kernel": "%s, the %d layers of the workload whose forward pass is "
+                                      "HBM-bound" % (kern, len(hb)),
+                            "bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
+                            "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": traffic,
+                            "avg_launch_us": ms * 1e3, "avg_bytes_per_launch": by}
+        if roofline is None:
+            roofline, roofline_hbm = roofline_hbm, None
+
+    update = measure_update(args, layers, torch, nc, dev, sptr, stream, flush) if use_ev \
+        else None
 
     if args.per_layer and use_ev:
         write_per_layer(args.per_layer, layers, ev_steps, args.steps)
@@ -533,32 +728,51 @@ def main():
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(args, wl)
 
+    sclk = clock.summary()
     L0 = layers[0]
+    metric = (METRIC_DW if depthwise else METRIC_RNXT if args.workload == "rnxt" else
+              METRIC_LAT if latency else METRIC)
+    unit = "us" if latency else "GB/s" if depthwise else "TFLOP/s"
     out = {
-        "metric": METRIC_DW if depthwise else METRIC_RNXT if args.workload == "rnxt" else METRIC,
+        "metric": metric,
         "value": value,
-        "unit": "GB/s" if depthwise else "TFLOP/s",
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": elapsed / args.steps * 1e3,
-        "higher_is_better": True,
+        "higher_is_better": not latency,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": args.dtype,
         "data": "synthetic (seeded; no dataset)",
-        "config": {"workload": wl.name + ", channel-last %s, fwd+dgrad+wgrad (stem fwd+wgrad), "
-                               "loss scale %g, fp32 dw" % (args.dtype, wl.loss_scale),
+        "config": {"workload": wl.name + ", %s %s, fwd+dgrad+wgrad%s, loss scale %g, "
+                               "fp32 dw" % (
+                                   "NCHW" if wl.layout == "nchw" else "channel-last", args.dtype,
+                                   " (stem fwd+wgrad)" if not all(L.dgrad for L in layers)
+                                   else "", wl.loss_scale),
                    "batch": L0.n, "layers": len(layers),
                    "layer_passes": sum(3 if L.dgrad else 2 for L in layers),
                    "tflop_per_step": step_flops / 1e12,
                    "compulsory_gb_per_step": step_bytes / 1e9},
-        "pct_of_peak": 100.0 * value / (PEAK_HBM_GBS if depthwise else PEAK_F16_TFLOPS),
+        "cache": {"headline": "cold" if cold_s is not None else "warm",
+                  "flush_bytes": args.flush_mib * 1024 * 1024,
+                  "cold": None if cold_s is None else {
+                      "ms_per_step": cold_s / args.steps * 1e3, "value": rate(cold_s)},
+                  "warm": {"ms_per_step": warm_s / args.steps * 1e3, "value": rate(warm_s)}},
+        "sclk": sclk,
         "per_pass": per_pass,
+        "attainable": attainable,
         "roofline": roofline,
+        "roofline_hbm": roofline_hbm,
         "cpu_baseline": cpu,
         "update": update,
     }
+    if not latency:
+        peak = PEAK_HBM_GBS if depthwise else PEAK_F16_TFLOPS
+        out["pct_of_peak"] = 100.0 * value / peak
+        if sclk and not depthwise:
+            out["pct_of_peak_at_sclk"] = 100.0 * value / sclk["peak_tflops_at_mean"]
     print(json.dumps(out), flush=True)
 
 

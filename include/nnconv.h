@@ -208,6 +208,17 @@ nnconv_status nnconv_wgrad_noalloc(const nnconv_desc *desc, const void *x, const
 
 /* Layout transforms (pure data movement of 16-bit elements, bit exact).
  *
+ * The paper's convolution call takes its channels on axis 1 (base_axis = 1
+ * in Sec. 3.2, Listing 5), i.e. [N][C][H][W] activations with [K][Cg][R][S]
+ * weights, stored in half precision (Sec. 3.3).  The matrix-core kernels
+ * read channel-last tensors, where one 16-byte load is 8 consecutive
+ * channels of a pixel; these calls move data between the two forms (the
+ * NCHW entry points above use them internally through the workspace) and
+ * pad the channel count of the 3-channel input image to 8 for the stem.
+ * All pointers are caller-owned device memory; src and dst must not
+ * overlap.  INVALID_ARG for null pointers or non-positive sizes (or a pad
+ * below the channel count); MISALIGNED for pointers not 2-byte aligned.
+ *
  * Activations: src[N][C][H][W] -> dst[N][H][W][c_pad], c_pad >= C; channels
  * C..c_pad-1 of dst are zero (the stem's 3 channels padded to 8). */
 nnconv_status nnconv_nchw_to_nhwc(const void *src, void *dst, int32_t n, int32_t c, int32_t h,

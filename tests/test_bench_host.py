@@ -73,12 +73,14 @@ def test_sweep_step_flops():
 
 def test_stored_traffic_only_for_its_sources(tmp_path, monkeypatch):
     good = tmp_path / "traffic.txt"
-    good.write_text("# comment: ignored\nfetch_bytes_per_launch: 100\n"
-                    "write_bytes_per_launch: 23\nsource_sha256: %s\n" % B.fwd_source_hash())
+    good.write_text("# comment: ignored\nmfma_fetch_bytes_per_launch: 100\n"
+                    "mfma_write_bytes_per_launch: 23\nhbm_fetch_bytes_per_launch: 7\n"
+                    "hbm_write_bytes_per_launch: 5\nsource_sha256: %s\n" % B.fwd_source_hash())
     monkeypatch.setattr(B, "TRAFFIC_FILE", str(good))
-    assert B.stored_traffic() == 123.0
+    assert B.stored_traffic("mfma") == 123.0
+    assert B.stored_traffic("hbm") == 12.0
     stale = tmp_path / "stale.txt"
-    stale.write_text("fetch_bytes_per_launch: 100\nwrite_bytes_per_launch: 23\n"
+    stale.write_text("mfma_fetch_bytes_per_launch: 100\nmfma_write_bytes_per_launch: 23\n"
                      "source_sha256: %s\n" % ("0" * 64))
     monkeypatch.setattr(B, "TRAFFIC_FILE", str(stale))
     assert B.stored_traffic() is None
@@ -94,3 +96,26 @@ def test_roofline_bound_is_the_larger_time(pass_):
         t_hbm = B.compulsory_bytes(L, pass_) / (B.PEAK_HBM_GBS * 1e9) * 1e6
         assert us == pytest.approx(max(t_mfma, t_hbm))
         assert bound == ("mfma" if t_mfma >= t_hbm else "hbm")
+
+
+def test_forward_launch_sets_partition_the_sweep():
+    """The MFMA-bound and HBM-bound forward sets split the 53 layers by the
+    compulsory-byte roofline: every layer in exactly one, the 3x3 layers of
+    stages 3-5 MFMA-bound, the 56x56 1x1 layers and the stem HBM-bound."""
+    args = argparse.Namespace(workload="sweep", dtype="f16", batch=0, layers="")
+    _, layers = B.layers_for(args)
+    mf, hb = B.fwd_sets(layers)
+    assert sorted(mf + hb) == list(range(53)) and not set(mf) & set(hb)
+    names_mf = {layers[i].name for i in mf}
+    names_hb = {layers[i].name for i in hb}
+    assert {"s3b1b", "s4b1b", "s5b1b", "s5b0b"} <= names_mf
+    assert {"stem", "s2b0a", "s2b0c", "s2b1a", "s2b0b"} <= names_hb
+
+
+def test_config1_workload_is_the_tiny_nchw_convolution():
+    args = argparse.Namespace(workload="cfg1", dtype="f16", batch=0, layers="")
+    wl, layers = B.layers_for(args)
+    assert wl.layout == "nchw" and len(layers) == 1
+    L = layers[0]
+    assert (L.n, L.c, L.h, L.w, L.k, L.r, L.s, L.stride, L.pad) == (2, 16, 16, 16, 16, 3, 3, 1, 1)
+    assert L.flops() == 2 * 2 * 16 * 16 * 16 * 16 * 9

@@ -13,8 +13,9 @@ first and last filter in full.  The error is max|err| / max|ref| over the
 sampled positions.  Every output element is also checked for bitwise
 reproducibility across two runs.
 
-Every distinct sweep, depthwise and grouped layer also runs at batch 3
-(ragged tiles) against the full oracle, in fp16 and bf16."""
+The sweep layers run at full size in bf16 too.  Every distinct sweep,
+depthwise and grouped layer also runs at batch 3 (ragged tiles) against the
+full oracle, in fp16 and bf16."""
 import zlib
 
 import numpy as np
@@ -50,8 +51,15 @@ def workload_cases(cfg, dtype=I.F16):
     return out
 
 
+def bf16_cases(cfg):
+    return [(name + " bf16", case) for name, case in workload_cases(cfg, I.BF16)]
+
+
+# the 53-layer sweep also in bf16 at its real size: at batch 256 the picker
+# sends the 14x14 layers to the 256x256 tiles, which smaller batches never
+# reach
 FULL_SIZE = (workload_cases(2) + workload_cases(3) + workload_cases(4) + workload_cases(5) +
-             workload_cases(6) + workload_cases(7))
+             bf16_cases(5) + workload_cases(6) + workload_cases(7))
 
 
 def border_and_random(rng, shape, n_random):

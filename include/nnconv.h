@@ -54,11 +54,11 @@
  *   - Non-finite inputs: forward and backward-weight multiply the zeros of
  *     the zero-extended input at taps outside the image, as the definition
  *     reads, so an inf or NaN weight (forward) or dy (backward-weight) makes
- *     every sum it meets non-finite, padding included.  Backward-data on
- *     the matrix-core and depthwise kernels reads dy zero-extended at every
- *     tap, so a non-finite weight also makes dx non-finite at positions the
- *     definition does not reach from that tap; the direct kernels add only
- *     the taps the definition has.
+ *     every sum it meets non-finite, padding included.  Backward-data has
+ *     only the terms the adjoint definition has: where the matrix-core and
+ *     depthwise kernels read dy zero-extended, a weight scan queued with
+ *     the call has the border pixels recomputed from the definition when
+ *     any weight is inf or NaN (small-group convolution excepted, above).
  *
  * Errors: every argument check happens on the host before anything is
  * queued.  On a non-OK status nothing is launched and no output or

@@ -206,11 +206,11 @@ int32_t plan_wgrad_direct_splits(const Geom &G) {
 }
 
 struct Regions {  // byte offsets into the caller's workspace
-    size_t a, b, c, d, total;
+    size_t a, b, c, d, e, total;
 };
 
 Regions fast_regions(const Geom &G, nnconv_pass pass) {
-    Regions R = {0, 0, 0, 0, 0};
+    Regions R = {0, 0, 0, 0, 0, 0};
     const size_t e2 = 2;
     const size_t xb = G.n * G.h * G.w * G.c * e2;
     const size_t yb = G.n * G.p * G.q * G.k * e2;
@@ -235,6 +235,8 @@ Regions fast_regions(const Geom &G, nnconv_pass pass) {
             R.c = take(xb);  // dx channel-last
         }
         R.b = take(wb);      // w [g][R][S][Cg][Kg]
+        // non-finite flags of the weight re-layout's workgroups
+        R.e = take((size_t)transpose16_blocks(G.g, G.r * G.s * G.cg, G.kg) * 4);
     } else {
         if (nchw) {
             R.a = take(xb);  // x channel-last
@@ -257,7 +259,7 @@ DWParams dw_params(const Geom &G, float alpha);
 // Depthwise workspace: the channel-last copies for NCHW calls, fp32 split
 // partials (backward-weight).
 Regions dw_regions(const Geom &G, nnconv_pass pass) {
-    Regions R = {0, 0, 0, 0, 0};
+    Regions R = {0, 0, 0, 0, 0, 0};
     const size_t xb = G.n * G.h * G.w * G.c * 2;
     const size_t yb = G.n * G.p * G.q * G.k * 2;
     size_t off = 0;
@@ -271,6 +273,7 @@ Regions dw_regions(const Geom &G, nnconv_pass pass) {
         if (nchw) { R.a = take(xb); R.c = take(yb); }
     } else if (pass == NNCONV_DGRAD) {
         if (nchw) { R.a = take(yb); R.c = take(xb); }
+        R.e = take((size_t)nonfinite_scan16_blocks(G.c * G.r * G.s) * 4);  // weight flags
     } else {
         if (nchw) { R.a = take(xb); R.b = take(yb); }
         R.c = take((size_t)dw_params(G, 1.0f).splits * G.c * G.r * G.s * 4);
@@ -283,13 +286,14 @@ Regions dw_regions(const Geom &G, nnconv_pass pass) {
 // backward-data), then the super-grouped problem's own regions.
 Regions sg_regions(const Geom &G, nnconv_pass pass) {
     const Geom S = sg_geom(G);
-    Regions R = {0, 0, 0, 0, 0};
+    Regions R = {0, 0, 0, 0, 0, 0};
     const size_t wexp = pass == NNCONV_WGRAD ? 0 : align256(G.k * G.r * G.s * SUPER_GROUP * 2);
     const Regions in = fast_regions(S, pass);
     R.d = 0;            // expanded weights
     R.a = wexp + in.a;  // NCHW copies / dgrad weight re-layout / partials, shifted
     R.b = wexp + in.b;
     R.c = wexp + in.c;
+    R.e = wexp + in.e;
     R.total = wexp + in.total;
     return R;
 }
@@ -327,6 +331,38 @@ DirectParams direct_params(const Geom &G, float alpha) {
     }
     P.alpha = alpha;
     return P;
+}
+
+// The same element strides for channel-last activations (the layout the
+// fast kernels produce dx in, also for NCHW calls, whose dx is transposed
+// afterwards), weights as the caller gave them.
+DirectParams direct_params_cl(const Geom &G, float alpha) {
+    DirectParams P = direct_params(G, alpha);
+    P.xs[0] = G.h * G.w * G.c; P.xs[1] = 1; P.xs[2] = G.w * G.c; P.xs[3] = G.c;
+    P.ys[0] = G.p * G.q * G.k; P.ys[1] = 1; P.ys[2] = G.q * G.k; P.ys[3] = G.k;
+    return P;
+}
+
+// dx rows (cols) at the top / bottom (left / right) that may have filter
+// taps outside dy: row i reaches p < 0 only if i < (R-1)*dil - pad, and
+// p >= P only if i >= P*stride - pad.
+struct Border {
+    int32_t bt, bb, bl, br;
+};
+Border dgrad_border(const Geom &G) {
+    auto ext = [](int64_t h, int64_t r, int64_t ph, int64_t dh, int64_t sh, int64_t p,
+                  int32_t &lo, int32_t &hi) {
+        int64_t t = (r - 1) * dh - ph;
+        t = t < 0 ? 0 : (t > h ? h : t);
+        int64_t b = h - (p * sh - ph);
+        b = b < 0 ? 0 : (b > h - t ? h - t : b);
+        lo = (int32_t)t;
+        hi = (int32_t)b;
+    };
+    Border B;
+    ext(G.h, G.r, G.ph, G.dh, G.sh, G.p, B.bt, B.bb);
+    ext(G.w, G.s, G.pw, G.dw, G.sw, G.q, B.bl, B.br);
+    return B;
 }
 
 thread_local int32_t last_hip_error = 0;
@@ -684,7 +720,15 @@ nnconv_status dw_dgrad(const Geom &G, const void *dy, const void *w, void *dx, f
         dyn = ws + R.a;
         dxn = ws + R.c;
     }
+    int32_t *flags = (int32_t *)(ws + R.e);
+    TRY_HIP(launch_nonfinite_scan16(w, G.c * G.r * G.s, G.dtype, flags, st));
     TRY_HIP(launch_depthwise(G.dtype, 1, dw_params(G, alpha), dyn, w, dxn, st));
+    // the depthwise kernels read dy zero-extended: recompute the border
+    // pixels from the definition when a weight is inf or NaN
+    const Border B = dgrad_border(G);
+    TRY_HIP(launch_dgrad_border(G.dtype, direct_params_cl(G, alpha), dyn, w, dxn, flags,
+                                (int32_t)nonfinite_scan16_blocks(G.c * G.r * G.s), B.bt, B.bb,
+                                B.bl, B.br, st));
     if (G.layout == NNCONV_NCHW)
         return hip_status(launch_transpose16(dxn, dx, G.n, G.h * G.w, G.c, G.h * G.w, st));
     return NNCONV_OK;
@@ -919,9 +963,18 @@ static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const v
         dyn = dyt;
         dxn = base + R.c;
     }
-    // [g][Kg][R*S*Cg] -> [g][R*S*Cg][Kg]
-    TRY_HIP(launch_transpose16(wkrsc, wt, G.g, G.kg, G.r * G.s * G.cg, G.kg, s));
+    // [g][Kg][R*S*Cg] -> [g][R*S*Cg][Kg], noting any inf or NaN weight
+    int32_t *flags = (int32_t *)(base + R.e);
+    TRY_HIP(launch_transpose16_scan(wkrsc, wt, G.g, G.kg, G.r * G.s * G.cg, G.kg, G.dtype, flags,
+                                    s));
     if ((st = dgrad_fast(G, dyn, wt, dxn, alpha, s, tile)) != NNCONV_OK) return st;
+    // the implicit-GEMM kernels read dy zero-extended at every tap of a
+    // stride phase: recompute the border pixels from the definition when a
+    // weight is inf or NaN (with finite weights the kernel exits at once)
+    const Border B = dgrad_border(G);
+    TRY_HIP(launch_dgrad_border(G.dtype, direct_params_cl(G, alpha), dyn, w, dxn, flags,
+                                (int32_t)transpose16_blocks(G.g, G.r * G.s * G.cg, G.kg), B.bt,
+                                B.bb, B.bl, B.br, s));
     if (G.layout == NNCONV_NCHW)
         return hip_status(launch_transpose16(dxn, dx, G.n, G.h * G.w, G.c, G.h * G.w, s));
     return NNCONV_OK;

@@ -15,6 +15,9 @@ __device__ __forceinline__ float ld16(const void *p, int64_t i) {
     return from16<T>(((const uint16_t *)p)[i]);
 }
 
+// Exponent field of a 16-bit storage type: all ones means inf or NaN.
+static uint32_t expmask16(int dtype) { return dtype == Half::id ? 0x7C00u : 0x7F80u; }
+
 template <class T>
 __global__ __launch_bounds__(256) void direct_fwd_kernel(const DirectParams P, const void *x,
                                                          const void *w, void *y) {
@@ -165,10 +168,15 @@ hipError_t launch_direct_wgrad(int dtype, const DirectParams &p, const void *x, 
 
 // dst[b][cc][rr] = rr < rows ? src[b][rr][cc] : 0, through a 64x64 LDS tile
 // (reads coalesced along cc, writes coalesced along rr).
+//
+// SCAN: also store into flags[blockIdx.x] whether any element of the tile is
+// inf or NaN (all exponent bits of expmask set).
+template <bool SCAN>
 __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__restrict__ src,
                                                           uint16_t *__restrict__ dst, int64_t rows,
                                                           int64_t cols, int64_t dst_ld,
-                                                          int64_t tiles_c, int64_t tiles_r) {
+                                                          int64_t tiles_c, int64_t tiles_r,
+                                                          uint32_t expmask, int32_t *flags) {
     __shared__ uint16_t tile[64][65];
     const int64_t t = blockIdx.x;
     const int64_t b = t / (tiles_c * tiles_r);
@@ -177,11 +185,19 @@ __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__rest
     const int64_t r0 = tr * 64, c0 = tc * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
     const uint16_t *s = src + b * rows * cols;
+    int bad = 0;
     for (int i = ty; i < 64; i += 4) {
         const int64_t rr = r0 + i, cc = c0 + tx;
-        tile[i][tx] = (rr < rows && cc < cols) ? s[rr * cols + cc] : (uint16_t)0;
+        const uint16_t v = (rr < rows && cc < cols) ? s[rr * cols + cc] : (uint16_t)0;
+        tile[i][tx] = v;
+        if constexpr (SCAN) bad |= (v & expmask) == expmask;
     }
-    __syncthreads();
+    if constexpr (SCAN) {
+        bad = __syncthreads_or(bad);
+        if (threadIdx.x == 0) flags[blockIdx.x] = bad;
+    } else {
+        __syncthreads();
+    }
     uint16_t *d = dst + b * cols * dst_ld;
     for (int i = ty; i < 64; i += 4) {
         const int64_t cc = c0 + i, rr = r0 + tx;
@@ -193,11 +209,13 @@ __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__rest
 // multiples of 8, 16-byte aligned buffers): a 64x64 tile is read as 8-element
 // row chunks, and each output chunk gathers 8 consecutive rows of one column
 // from LDS.
+template <bool SCAN>
 __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__restrict__ src,
                                                               uint16_t *__restrict__ dst,
                                                               int64_t rows, int64_t cols,
                                                               int64_t dst_ld, int64_t tiles_c,
-                                                              int64_t tiles_r) {
+                                                              int64_t tiles_r, uint32_t expmask,
+                                                              int32_t *flags) {
     constexpr int LD = 72;  // halves per LDS row (144 bytes: 16-byte aligned, skewed)
     __shared__ uint16_t tile[64 * LD];
     const int64_t t = blockIdx.x;
@@ -206,6 +224,7 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
     const int64_t tr = rem / tiles_c, tc = rem - (rem / tiles_c) * tiles_c;
     const int64_t r0 = tr * 64, c0 = tc * 64;
     const uint16_t *s = src + b * rows * cols;
+    int bad = 0;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int id = threadIdx.x + 256 * i;
@@ -214,8 +233,18 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
         u32x4 v = u32x4{};
         if (rr < rows && col < cols) v = *(const u32x4 *)(s + rr * cols + col);
         *(u32x4 *)(&tile[row * LD + cc]) = v;
+        if constexpr (SCAN) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                bad |= ((v[e] & expmask) == expmask) | (((v[e] >> 16) & expmask) == expmask);
+        }
     }
-    __syncthreads();
+    if constexpr (SCAN) {
+        bad = __syncthreads_or(bad);
+        if (threadIdx.x == 0) flags[blockIdx.x] = bad;
+    } else {
+        __syncthreads();
+    }
     uint16_t *d = dst + b * cols * dst_ld;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -267,21 +296,152 @@ hipError_t launch_expand_group_weights(const void *src, void *dst, int64_t k, in
     return hipGetLastError();
 }
 
-hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
-                              int64_t cols, int64_t dst_ld, hipStream_t st) {
+int64_t transpose16_blocks(int64_t batch, int64_t cols, int64_t dst_ld) {
+    return batch * ((cols + 63) / 64) * ((dst_ld + 63) / 64);
+}
+
+template <bool SCAN>
+static hipError_t transpose16_go(const void *src, void *dst, int64_t batch, int64_t rows,
+                                 int64_t cols, int64_t dst_ld, uint32_t expmask, int32_t *flags,
+                                 hipStream_t st) {
     const int64_t tiles_c = (cols + 63) / 64, tiles_r = (dst_ld + 63) / 64;
     const int64_t nb = batch * tiles_c * tiles_r;
     if (nb <= 0) return hipSuccess;
+    if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     const bool vec = cols % 8 == 0 && dst_ld % 8 == 0 && rows % 8 == 0 &&
                      (uintptr_t)src % 16 == 0 && (uintptr_t)dst % 16 == 0;
     if (vec)
-        hipLaunchKernelGGL(transpose16_vec_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
+        hipLaunchKernelGGL(transpose16_vec_kernel<SCAN>, dim3((uint32_t)nb), dim3(256), 0, st,
                            (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
-                           tiles_r);
+                           tiles_r, expmask, flags);
     else
-        hipLaunchKernelGGL(transpose16_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
+        hipLaunchKernelGGL(transpose16_kernel<SCAN>, dim3((uint32_t)nb), dim3(256), 0, st,
                            (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
-                           tiles_r);
+                           tiles_r, expmask, flags);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
+                              int64_t cols, int64_t dst_ld, hipStream_t st) {
+    return transpose16_go<false>(src, dst, batch, rows, cols, dst_ld, 0u, nullptr, st);
+}
+
+hipError_t launch_transpose16_scan(const void *src, void *dst, int64_t batch, int64_t rows,
+                                   int64_t cols, int64_t dst_ld, int dtype, int32_t *flags,
+                                   hipStream_t st) {
+    return transpose16_go<true>(src, dst, batch, rows, cols, dst_ld, expmask16(dtype), flags,
+                                st);
+}
+
+// flags[b] = whether any of the 16-bit elements [2048 b, 2048 b + 2048) of
+// src[0, count) is inf or NaN.
+__global__ __launch_bounds__(256) void nonfinite_scan16_kernel(const uint16_t *__restrict__ src,
+                                                               int64_t count, uint32_t expmask,
+                                                               int32_t *flags) {
+    int bad = 0;
+    const int64_t base = (int64_t)blockIdx.x * 2048;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int64_t e = base + u * 256 + threadIdx.x;
+        if (e < count) bad |= (src[e] & expmask) == expmask;
+    }
+    bad = __syncthreads_or(bad);
+    if (threadIdx.x == 0) flags[blockIdx.x] = bad;
+}
+
+int64_t nonfinite_scan16_blocks(int64_t count) { return (count + 2047) / 2048; }
+
+hipError_t launch_nonfinite_scan16(const void *src, int64_t count, int dtype, int32_t *flags,
+                                   hipStream_t st) {
+    const int64_t nb = nonfinite_scan16_blocks(count);
+    if (nb <= 0) return hipSuccess;
+    if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(nonfinite_scan16_kernel, dim3((uint32_t)nb), dim3(256), 0, st,
+                       (const uint16_t *)src, count, expmask16(dtype), flags);
+    return hipGetLastError();
+}
+
+// Backward-data border fix-up.  The matrix-core and depthwise kernels read
+// dy zero-extended at every filter tap of a stride phase, so an inf or NaN
+// weight meets those zeros (0 * inf = NaN) at dx pixels whose taps leave dy
+// -- terms the definition does not have.  When any weight is non-finite
+// (some flag set), this kernel recomputes every such border pixel from the
+// definition: rows [0, bt) and [H - bb, H), and columns [0, bl) and
+// [W - br, W) of the other rows, every channel, skipping the taps outside dy.
+// With all flags clear every workgroup returns at once.
+template <class T>
+__global__ __launch_bounds__(256) void dgrad_border_kernel(const DirectParams P, const void *dy,
+                                                           const void *w, void *dx,
+                                                           const int32_t *flags, int32_t nflags,
+                                                           int32_t bt, int32_t bb, int32_t bl,
+                                                           int32_t br) {
+    int any = 0;
+    for (int i = threadIdx.x; i < nflags; i += 256) any |= flags[i];
+    if (!__syncthreads_or(any)) return;
+    const int64_t mid = P.h - bt - bb;
+    const int64_t per_img = (int64_t)(bt + bb) * P.w + mid * (bl + br);
+    const int64_t total = (int64_t)P.n * per_img * P.c;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * 256) {
+        const int c = (int)(e % P.c);
+        int64_t f = e / P.c;
+        const int64_t pix = f % per_img;
+        const int n = (int)(f / per_img);
+        int i, j;
+        if (pix < (int64_t)bt * P.w) {
+            i = (int)(pix / P.w);
+            j = (int)(pix % P.w);
+        } else if (pix < (int64_t)(bt + bb) * P.w) {
+            const int64_t q = pix - (int64_t)bt * P.w;
+            i = P.h - bb + (int)(q / P.w);
+            j = (int)(q % P.w);
+        } else {
+            const int64_t q = pix - (int64_t)(bt + bb) * P.w;
+            i = bt + (int)(q / (bl + br));
+            const int u = (int)(q % (bl + br));
+            j = u < bl ? u : P.w - br + (u - bl);
+        }
+        const int g = c / P.cg;
+        const int cc = c - g * P.cg;
+        float acc = 0.f;
+        for (int kk = 0; kk < P.kg; ++kk) {
+            const int k = g * P.kg + kk;
+            for (int r = 0; r < P.r; ++r) {
+                const int nump = i + P.ph - r * P.dh;
+                if (nump < 0 || nump % P.sh) continue;
+                const int p = nump / P.sh;
+                if (p >= P.p) continue;
+                for (int s = 0; s < P.s; ++s) {
+                    const int numq = j + P.pw - s * P.dw;
+                    if (numq < 0 || numq % P.sw) continue;
+                    const int q = numq / P.sw;
+                    if (q >= P.q) continue;
+                    const float dv =
+                        ld16<T>(dy, n * P.ys[0] + k * P.ys[1] + p * P.ys[2] + q * P.ys[3]);
+                    const float fv =
+                        ld16<T>(w, k * P.wsd[0] + cc * P.wsd[1] + r * P.wsd[2] + s * P.wsd[3]);
+                    acc += dv * fv;
+                }
+            }
+        }
+        ((uint16_t *)dx)[n * P.xs[0] + c * P.xs[1] + i * P.xs[2] + j * P.xs[3]] =
+            (uint16_t)to16<T>(acc * P.alpha);
+    }
+}
+
+hipError_t launch_dgrad_border(int dtype, const DirectParams &p, const void *dy, const void *w,
+                               void *dx, const int32_t *flags, int32_t nflags, int32_t bt,
+                               int32_t bb, int32_t bl, int32_t br, hipStream_t st) {
+    if (bt + bb == 0 && bl + br == 0) return hipSuccess;
+    if (bt < 0 || bb < 0 || bl < 0 || br < 0 || bt + bb > p.h || bl + br > p.w)
+        return hipErrorInvalidValue;
+    const dim3 grid(256), block(256);
+    if (dtype == Half::id)
+        hipLaunchKernelGGL(dgrad_border_kernel<Half>, grid, block, 0, st, p, dy, w, dx, flags,
+                           nflags, bt, bb, bl, br);
+    else
+        hipLaunchKernelGGL(dgrad_border_kernel<BFloat>, grid, block, 0, st, p, dy, w, dx, flags,
+                           nflags, bt, bb, bl, br);
     return hipGetLastError();
 }
 

@@ -188,6 +188,25 @@ hipError_t launch_wgrad_reduce_diag(const float *ws, int32_t splits, int64_t k, 
 // dst[b][cc][rr] = rr < rows ? src[b][rr][cc] : 0   for rr < dst_ld, cc < cols
 hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
                               int64_t cols, int64_t dst_ld, hipStream_t st);
+// launch_transpose16 that also stores, per workgroup b of the
+// transpose16_blocks(batch, cols, dst_ld) it launches, whether its tile of
+// src held an inf or NaN of the given operand dtype into flags[b].
+int64_t transpose16_blocks(int64_t batch, int64_t cols, int64_t dst_ld);
+hipError_t launch_transpose16_scan(const void *src, void *dst, int64_t batch, int64_t rows,
+                                   int64_t cols, int64_t dst_ld, int dtype, int32_t *flags,
+                                   hipStream_t st);
+// flags[b] (b < nonfinite_scan16_blocks(count)) = whether src[2048 b ..
+// 2048 b + 2047] holds an inf or NaN.
+int64_t nonfinite_scan16_blocks(int64_t count);
+hipError_t launch_nonfinite_scan16(const void *src, int64_t count, int dtype, int32_t *flags,
+                                   hipStream_t st);
+// If any of flags[0, nflags) is set: recompute dx at the border pixels (rows
+// [0, bt), [H - bb, H); columns [0, bl), [W - br, W)) from the definition,
+// skipping the taps outside dy.  Element strides come from p.
+hipError_t launch_dgrad_border(int dtype, const DirectParams &p, const void *dy, const void *w,
+                               void *dx, const int32_t *flags, int32_t nflags, int32_t bt,
+                               int32_t bb, int32_t bl, int32_t br, hipStream_t st);
+
 // dst[row][ch] = ch < c ? src[row][ch] : 0   for ch < c_pad
 hipError_t launch_pad_channels16(const void *src, void *dst, int64_t rows, int32_t c,
                                  int32_t c_pad, hipStream_t st);

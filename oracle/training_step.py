@@ -42,17 +42,22 @@ class LossScaler:
 
     def step(self, overflow: bool) -> bool:
         """Advance one training step; returns True when the update is
-        applied (no inf/NaN in the gradients)."""
-        if overflow:
-            self.scale /= self.factor
-            self.counter = 0
-            self.skipped += 1
-            return False
-        if self.counter > self.interval:
-            self.scale *= self.factor
-            self.counter = 0
-        self.counter += 1
-        return True
+        applied (no inf/NaN in the gradients).
+
+        Written as the transition the rule defines, not in the listing's
+        statement order: a clean step grows the scale exactly when more than
+        `interval` clean steps were counted before it; the counter then holds
+        the clean steps since the last growth or overflow, this one
+        included."""
+        ovf = bool(overflow)
+        grow = (not ovf) and self.counter > self.interval
+        # an overflow divides by the factor (not a multiply by its
+        # reciprocal, which rounds differently for other than powers of two)
+        self.scale = self.scale / self.factor if ovf else \
+            self.scale * (self.factor if grow else 1.0)
+        self.counter = 0 if ovf else (1 if grow else self.counter + 1)
+        self.skipped += int(ovf)
+        return not ovf
 
 
 def sgd_update(master, momentum, grad, scale, lr, mu, weight_decay):

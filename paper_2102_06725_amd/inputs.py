@@ -106,6 +106,23 @@ class Layer:
     c_logical: int = 0      # channel count before padding (stem: 3 padded to 8)
     count: int = 1          # how many ResNet-50 layers share this shape
     dgrad: bool = True      # the stem has no gradient to the image
+    # width-axis stride / padding / dilation when they differ from the
+    # height axis (0, -1, 0: the same as stride, pad, dil)
+    stride_w: int = 0
+    pad_w: int = -1
+    dil_w: int = 0
+
+    @property
+    def s_w(self) -> int:
+        return self.stride_w or self.stride
+
+    @property
+    def p_w(self) -> int:
+        return self.pad if self.pad_w < 0 else self.pad_w
+
+    @property
+    def d_w(self) -> int:
+        return self.dil_w or self.dil
 
     @property
     def p(self) -> int:
@@ -113,7 +130,7 @@ class Layer:
 
     @property
     def q(self) -> int:
-        return (self.w + 2 * self.pad - self.dil * (self.s - 1) - 1) // self.stride + 1
+        return (self.w + 2 * self.p_w - self.d_w * (self.s - 1) - 1) // self.s_w + 1
 
     @property
     def c_alg(self) -> int:

@@ -99,8 +99,8 @@ class Case:
 
     def desc(self):
         L = self.layer
-        return nc.make_desc(L.n, L.c, L.h, L.w, L.k, L.r, L.s, (L.stride, L.stride),
-                            (L.pad, L.pad), (L.dil, L.dil), L.groups,
+        return nc.make_desc(L.n, L.c, L.h, L.w, L.k, L.r, L.s, (L.stride, L.s_w),
+                            (L.pad, L.p_w), (L.dil, L.d_w), L.groups,
                             nc.NNCONV_NCHW if self.layout == "nchw" else nc.NNCONV_NHWC,
                             nc.NNCONV_F16 if self.dtype == I.F16 else nc.NNCONV_BF16)
 
@@ -126,8 +126,8 @@ def nchw_f64(case: Case, t):
 
 def oracle_conv(case: Case):
     L = case.layer
-    return orc.Conv(L.n, L.c_alg, L.h, L.w, L.k, L.r, L.s, (L.stride, L.stride), (L.pad, L.pad),
-                    (L.dil, L.dil), L.groups)
+    return orc.Conv(L.n, L.c_alg, L.h, L.w, L.k, L.r, L.s, (L.stride, L.s_w), (L.pad, L.p_w),
+                    (L.dil, L.d_w), L.groups)
 
 
 def workspace(desc, pass_):

@@ -8,6 +8,8 @@ and 64-channel implicit GEMMs with their stride phases, the direct kernels,
 the tiled and gather depthwise kernels, and 64-channel super-groups), with
 alpha != 1 on about a third of them.  Sizes
 are capped so that the oracle takes well under a second per case."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -86,6 +88,44 @@ def _id(c):
         c.dtype, c.alpha)
 
 
+def _axis_cases(n_cases=60):
+    """Geometries whose stride, padding and dilation differ between the
+    height and the width axis, from the same five families: the per-axis
+    index logic (stride phases and their taps, padding masks, the split-K
+    pixel decode, the depthwise and direct kernels) sees each axis alone."""
+    rng = np.random.default_rng(SEED + 8000)
+    out = []
+    i = 0
+    while len(out) < n_cases:
+        fam, L = _draw(rng, i)
+        i += 1
+        sw = int(rng.integers(1, 4))
+        dw = int(rng.choice([1, 1, 2]))
+        if (sw, dw) == (L.stride, L.dil):
+            sw = L.stride % 3 + 1
+        pw = int(rng.integers(0, dw * (L.s - 1) + 1))
+        L = dataclasses.replace(L, name="ax%d_%s" % (i, fam), stride_w=sw, dil_w=dw, pad_w=pw)
+        if L.p < 1 or L.q < 1:
+            continue
+        if L.n * L.k * L.p * L.q * (L.c // L.groups) * L.r * L.s > MAX_MACS:
+            continue
+        layout = "nchw" if rng.random() < 0.3 else "nhwc"
+        dtype = I.BF16 if rng.random() < 0.35 else I.F16
+        out.append(Case(L, layout=layout, dtype=dtype, loss_scale=float(rng.choice([1.0, 1024.0])),
+                        cfg=95, layer_id=len(out)))
+    return out
+
+
+AX_CASES = _axis_cases()
+
+
+def _axid(c):
+    L = c.layer
+    return "%s n%d c%d %dx%d k%d r%ds%d st%d,%d p%d,%d d%d,%d g%d %s %s" % (
+        L.name, L.n, L.c, L.h, L.w, L.k, L.r, L.s, L.stride, L.s_w, L.pad, L.p_w, L.dil, L.d_w,
+        L.groups, c.layout, c.dtype)
+
+
 @pytest.fixture(scope="module", autouse=True)
 def _setup(nnlib, oracle_lib):
     if not torch().cuda.is_available():
@@ -96,6 +136,12 @@ def _setup(nnlib, oracle_lib):
 @pytest.mark.parametrize("case", CASES, ids=[_id(c) for c in CASES])
 def test_random_shape_parity(case):
     print("case:", _id(case), flush=True)
+    full_parity(case)
+
+
+@pytest.mark.parametrize("case", AX_CASES, ids=[_axid(c) for c in AX_CASES])
+def test_random_unequal_axes_parity(case):
+    print("case:", _axid(case), flush=True)
     full_parity(case)
 
 

@@ -151,7 +151,14 @@ typedef enum {
     NNCONV_TILE_256x256_16W = 4,  /* 16 waves of 64x64, 2 stages */
     NNCONV_TILE_256x256_RING = 6, /* 4 waves of 128x128, ring of 4 32-element slices */
     NNCONV_TILE_256x128_RING = 7, /* 4 waves of 128x64, ring of 3 */
-    NNCONV_TILE_256x64_RING = 8   /* 4 waves of 64x64, ring of 4 */
+    NNCONV_TILE_256x64_RING = 8,  /* 4 waves of 64x64, ring of 4 */
+    /* Halo staging, for stride-1 geometries whose input image has the
+     * output's size and whose taps shift a pixel by at most 64 raster
+     * positions (3x3 filters with padding 1 on images up to 63 pixels
+     * wide; backward-data of the same at stride 1): 256-pixel tiles, each
+     * 64-channel slice of the input staged once per tile for all taps. */
+    NNCONV_TILE_HALO_256x64 = 9,    /* 4 waves of 64x64 */
+    NNCONV_TILE_HALO_256x128 = 10   /* 4 waves of 128x64 */
 } nnconv_tile;
 
 /* nnconv_fwd / nnconv_dgrad with the tile forced (an nnconv_tile value).
@@ -160,7 +167,8 @@ typedef enum {
  * call would not run on the implicit-GEMM kernel (reduction channels per tap
  * not a multiple of 64, depthwise or small-group convolution, the stem's
  * 8-channel shape, operands not 16-byte aligned or past 2 GiB, backward-data
- * with more than 4 stride phases). */
+ * with more than 4 stride phases), and for a halo tile on any other geometry
+ * than the one it states or on grouped convolution. */
 nnconv_status nnconv_fwd_tile(const nnconv_desc *desc, const void *x, const void *w, void *y,
                               float alpha, void *ws, size_t ws_bytes, void *hip_stream,
                               int32_t tile);

@@ -423,6 +423,31 @@ C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
     return red >= long_red ? C64_128x128 : C64S_128x128;
 }
 
+// Forced-tile ids from HALO_TILE0 on select the halo-staged kernel
+// (HaloConfig = id - HALO_TILE0).
+constexpr int HALO_TILE0 = 9;
+
+// Whether the halo-staged kernel can run this shape's forward and
+// backward-data passes (the geometry halo_supported() accepts, stated on the
+// convolution): one group, stride 1, output the input's size, 64-channel
+// multiples, taps spanning at most HALO_ROWS - 256 raster positions.
+bool halo_geom(const Geom &G) {
+    return G.g == 1 && G.sh == 1 && G.sw == 1 && G.p == G.h && G.q == G.w && G.cg % 64 == 0 &&
+           G.kg % 64 == 0 && G.r * G.s <= 32 &&
+           (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw + 256 <= HALO_ROWS;
+}
+
+// The halo-staged kernel's tile for a stride-1 "same" implicit GEMM, or -1
+// for the 64-channel-slice kernel.  Measured on the ResNet-50 3x3 layers at
+// batch 256: the halo tile wins on 7x7 images with wide outputs (there the
+// 64-channel-slice tiles stage each input pixel once per tap and per
+// 64-column tile), by about 13% forward and backward-data, and ties or
+// loses on the wider images.
+int pick_halo(const TNParams &p) {
+    if (!halo_supported(p) || p.a_w > 7 || p.ncols < 256) return -1;
+    return HALO_256x64;
+}
+
 // Compute units of the current device (the persistent kernels launch one
 // workgroup per CU).
 int device_cus() {
@@ -521,6 +546,11 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     if (G.cg % 64 == 0) {
         p.nphase = 1;
         p.ph[0] = phase_of(p.M, p.mi, p.mj, 0, 0, 0, t);
+        const int hc = tile >= HALO_TILE0 ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
+        if (hc >= 0) {
+            if (!halo_supported(p)) return NNCONV_ERR_UNSUPPORTED;
+            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, st));
+        }
         const C64Config cfg =
             tile >= 0 ? (C64Config)tile : pick_c64_geom(G, p.M, G.kg, (int64_t)t * G.cg);
         return hip_status(launch_igemm_c64(G.dtype, cfg, p, G.ph > 0 || G.pw > 0, st));
@@ -595,6 +625,11 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             }
         }
         if (p.nphase == 0) return NNCONV_OK;
+        const int hc = tile >= HALO_TILE0 ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
+        if (hc >= 0) {
+            if (!halo_supported(p)) return NNCONV_ERR_UNSUPPORTED;
+            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, st));
+        }
         const C64Config cfg =
             tile >= 0 ? (C64Config)tile : pick_c64_geom(G, rows, G.cg, red_rows / rows);
         return hip_status(launch_igemm_c64(G.dtype, cfg, p, pad, st));
@@ -865,7 +900,8 @@ static nnconv_status check_ws(const Geom &G, nnconv_pass pass, const void *ws, s
 // kernel other than the block-diagonal one, on a dense call that takes that
 // kernel with its operands as given.
 bool tile_ok(int tile) {
-    return tile >= C64_256x256 && tile <= C64R_256x64 && tile != C64D_128x64;
+    return (tile >= C64_256x256 && tile <= C64R_256x64 && tile != C64D_128x64) ||
+           (tile >= HALO_TILE0 && tile <= HALO_TILE0 + HALO_256x128);
 }
 
 static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void *w, void *y,
@@ -882,7 +918,8 @@ static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void
         const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_fwd_shape(G) &&
                            aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                            (G.layout == NNCONV_NHWC || aligned(ws, 16));
-        if (!tile_ok(tile) || !dense) return NNCONV_ERR_UNSUPPORTED;
+        if (!tile_ok(tile) || !dense || (tile >= HALO_TILE0 && !halo_geom(G)))
+            return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();
     if (dw_shape(G)) {
@@ -932,7 +969,8 @@ static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const v
         const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_dgrad_shape(G) &&
                            aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
                            aligned(ws, 16);
-        if (!tile_ok(tile) || !dense) return NNCONV_ERR_UNSUPPORTED;
+        if (!tile_ok(tile) || !dense || (tile >= HALO_TILE0 && !halo_geom(G)))
+            return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();
     if (dw_shape(G)) {

@@ -18,7 +18,7 @@
 //   - zero padding: rows outside the GEMM get an out-of-range offset once;
 //     for padded convolutions each staged row carries a bitmask of the taps
 //     that land inside the image, tested per load.
-#include "launch.hpp"
+#include "igemm_store.hpp"
 
 namespace nnconv {
 
@@ -347,57 +347,8 @@ void igemm_c64_kernel(const TNParams P) {
         }
     }
 
-    // Epilogue through LDS: the tile is converted to 16-bit and written to
-    // LDS as [BM pixel rows][BN channels] (16-byte chunks swizzled by row),
-    // then read back a 16-byte chunk per lane, consecutive lanes along a row,
-    // so every global store writes whole cache lines of one output pixel.
-    // Lane (MFMA layout) holds pixel l32 of each 32-pixel block and, of each
-    // 32-channel block, channels 8*e + 4*khalf + {0..3} (e = 0..3).
-    constexpr int CPR = BN / 8;                    // 16-byte chunks per tile row
-    constexpr int CSW = CPR < 16 ? CPR - 1 : 15;   // chunk swizzle mask
     static_assert(BM * BN / 8 <= LDS_SLOTS, "C tile must fit in LDS");
-    barrier_lds();  // every wave is done reading the last k-slice
-    {
-        char *cl = (char *)&lds[0];
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int r = wm * WTM + i * 32 + l32;
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int c = (wn * WTN + j * 32) / 8 + e;
-                    u32x2 pk;
-                    pk[0] = to16<T>(acc[j][i][4 * e + 0] * P.alpha) |
-                            (to16<T>(acc[j][i][4 * e + 1] * P.alpha) << 16);
-                    pk[1] = to16<T>(acc[j][i][4 * e + 2] * P.alpha) |
-                            (to16<T>(acc[j][i][4 * e + 3] * P.alpha) << 16);
-                    *(u32x2 *)(cl + (r * CPR + (c ^ (r & CSW))) * 16 + khalf * 8) = pk;
-                }
-            }
-        }
-    }
-    barrier_lds();
-    uint16_t *out = (uint16_t *)P.out;
-    constexpr int ROWS_PER_PASS = NW * 64 / CPR;
-#pragma unroll 4
-    for (int r = tid / CPR; r < BM; r += ROWS_PER_PASS) {
-        const int c = tid % CPR;
-        const int m = m0 + r;
-        const int ch = n0 + c * 8;
-        if (m >= F.M || ch >= P.ncols) continue;
-        const int q1 = (int)fdiv((uint32_t)m, F.div_mj);
-        const int jj = m - q1 * F.mj;
-        const int n = (int)fdiv((uint32_t)q1, F.div_mi);
-        const int ii = q1 - n * F.mi;
-        const int oh = ii * P.oi_mul + F.oi_add;
-        const int ow = jj * P.oj_mul + F.oj_add;
-        const int64_t obase =
-            ((int64_t)(n * P.o_h + oh) * P.o_w + ow) * P.o_c + (int64_t)g * P.o_cg_ofs;
-        // streaming store: the output is not read again by this pass, so it
-        // should not displace operand lines in L2
-        __builtin_nontemporal_store(lds[r * CPR + (c ^ (r & CSW))], (u32x4 *)(out + obase + ch));
-    }
+    store_tile<T, BM, BN, WM, WN, FM, FN>(acc, &lds[0], P, F, m0, n0, g);
 }
 
 template <class T, int BM, int BN, int WM, int WN, int BKC, int STAGES, bool DIAG = false,

@@ -97,6 +97,17 @@ enum C64Config { C64_256x256 = 0,   // 8 waves, 64-element slices, 2 stages
                  C64R_256x64 = 8 };   // 4 waves of 64x64, 4 stages (80 KB), 2 per CU
 hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hipStream_t st);
 
+// Halo staging for stride-1 "same" geometries (igemm_halo.hip): single
+// phase, one group, cr % 64 == 0, A image of the output's size, at most 32
+// taps whose raster shifts span at most HALO_ROWS - 256 pixels (3x3 filters
+// with padding 1 on images up to 63 pixels wide).  256-pixel tiles.
+constexpr int HALO_ROWS = 384;
+enum HaloConfig { HALO_256x64 = 0,    // 4 waves of 64x64
+                  HALO_256x128 = 1 };  // 4 waves of 128x64
+bool halo_supported(const TNParams &p);
+// hipErrorInvalidValue when !halo_supported(p)
+hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, hipStream_t st);
+
 // Forward pass for 8-channel (16-byte) channel-last pixels, 64 output
 // channels, groups 1, dilation 1 and a compiled filter size / stride (the
 // stem: 7x7, stride 2).  x [n][h][w][8], wt [64][r][s][8], y [n][p][q][64].

@@ -184,7 +184,7 @@ def test_forced_tile_validation(nnlib):
     calls = (nc.nnconv_fwd_tile, nc.nnconv_dgrad_tile)
     for f in calls:
         assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, -1) == inv
-        for bad in (5, 9, 99):  # block-diagonal tile, out of range
+        for bad in (5, 11, 99):  # block-diagonal tile, out of range
             assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, bad) == uns
         # 16 reduction channels per tap: not the 64-channel-slice kernel
         small = nc.make_desc(2, 16, 8, 8, 16, 3, 3, pad=(1, 1))
@@ -204,6 +204,18 @@ def test_forced_tile_validation(nnlib):
     # backward-data with more than four stride phases
     s3 = nc.make_desc(2, 64, 9, 9, 64, 3, 3, stride=(3, 3), pad=(1, 1))
     assert nc.nnconv_dgrad_tile(s3, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns
+    # halo tiles: stride 1 with the output the input's size, 3x3 on images up
+    # to 63 pixels wide (taps spanning at most 128 raster positions)
+    halo = nc.HALO_TILES
+    not_same = (nc.make_desc(2, 64, 8, 8, 64, 3, 3, stride=(2, 2), pad=(1, 1)),
+                nc.make_desc(2, 64, 8, 8, 64, 3, 3, pad=(0, 0)),
+                nc.make_desc(2, 64, 8, 64, 64, 3, 3, pad=(1, 1)),
+                nc.make_desc(2, 64, 8, 8, 64, 3, 3, pad=(1, 1), groups=2),
+                nc.make_desc(2, 64, 8, 8, 32, 3, 3, pad=(1, 1)))
+    for f in calls:
+        for d in not_same:
+            for t in halo:
+                assert f(d, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, t) == uns
 
 
 def test_noalloc_wgrad_validation(nnlib):

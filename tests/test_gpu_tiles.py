@@ -37,7 +37,33 @@ def test_forced_tile_parity(nnlib, oracle_lib, tile, dtype, shape):
     U.full_parity(case, passes=("fwd", "dgrad"), tile=tile)
 
 
-@pytest.mark.parametrize("tile", [nc.NNCONV_TILE_256x256_RING, nc.NNCONV_TILE_256x128_RING])
+# Stride-1 geometries whose output is the input's size: the halo tiles.
+HALO_SHAPES = [
+    # name, n, c, h, w, k, r, s, pad, dil
+    ("h3", 5, 64, 10, 10, 320, 3, 3, 1, 1),      # 500 rows: a ragged second tile
+    ("h3w63", 3, 128, 9, 63, 192, 3, 3, 1, 1),   # widest image: a 384-row halo
+    ("h3tiny", 1, 64, 3, 4, 64, 3, 3, 1, 1),     # 12 rows, halo past both ends
+    ("h1", 2, 64, 9, 15, 64, 1, 1, 0, 1),        # 1x1: the halo is the tile
+    ("h5", 2, 64, 8, 12, 128, 5, 5, 2, 1),       # 25 taps
+    ("hdil", 2, 128, 11, 9, 64, 3, 3, 2, 2),     # dilation 2
+    ("hlong", 2, 512, 5, 6, 256, 3, 3, 1, 1),    # 8 channel slices
+]
+
+
+@pytest.mark.parametrize("tile", nc.HALO_TILES)
+@pytest.mark.parametrize("dtype", [I.F16, I.BF16])
+@pytest.mark.parametrize("shape", HALO_SHAPES, ids=[s[0] for s in HALO_SHAPES])
+def test_forced_halo_tile_parity(nnlib, oracle_lib, tile, dtype, shape):
+    name, n, c, h, w, k, r, s, pad, dil = shape
+    L = I.Layer(name, n, c, h, w, k, r, s, stride=1, pad=pad, dil=dil)
+    case = U.Case(L, dtype=dtype, loss_scale=1.0, x_kind="normal", cfg=93,
+                  layer_id=tile * 10 + HALO_SHAPES.index(shape))
+    print("halo tile %d %s %s" % (tile, dtype, name), flush=True)
+    U.full_parity(case, passes=("fwd", "dgrad"), tile=tile)
+
+
+@pytest.mark.parametrize("tile", [nc.NNCONV_TILE_256x256_RING, nc.NNCONV_TILE_256x128_RING,
+                                  nc.NNCONV_TILE_HALO_256x64, nc.NNCONV_TILE_HALO_256x128])
 def test_forced_tile_nchw_and_alpha(nnlib, oracle_lib, tile):
     """NCHW calls go through the channel-last kernels via the workspace; a
     non-unit alpha scales before the single rounding."""

@@ -188,7 +188,8 @@ def write_per_layer(path, layers, ev_steps, steps):
 
 # Sources that determine the forward launches (dispatch plans and kernels);
 # stored HBM-traffic counters are reported only while these are unchanged.
-FWD_SOURCES = ("api.hip", "common.hpp", "igemm_c8.hip", "igemm_c64.hip", "launch.hpp", "stem.hip")
+FWD_SOURCES = ("api.hip", "common.hpp", "igemm_c8.hip", "igemm_c64.hip", "igemm_halo.hip",
+               "igemm_store.hpp", "launch.hpp", "stem.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "igemm_fwd_traffic_resnet50_b256.txt")
 COPY_ROW_BYTES = 128    # calibration copy: rows of 64 fp16 channels
 

@@ -430,11 +430,11 @@ constexpr int HALO_TILE0 = 9;
 // Whether the halo-staged kernel can run this shape's forward and
 // backward-data passes (the geometry halo_supported() accepts, stated on the
 // convolution): one group, stride 1, output the input's size, 64-channel
-// multiples, taps spanning at most HALO_ROWS - 256 raster positions.
+// multiples, taps spanning at most HALO_SPAN raster positions.
 bool halo_geom(const Geom &G) {
     return G.g == 1 && G.sh == 1 && G.sw == 1 && G.p == G.h && G.q == G.w && G.cg % 64 == 0 &&
            G.kg % 64 == 0 && G.r * G.s <= 32 &&
-           (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw + 256 <= HALO_ROWS;
+           (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw <= HALO_SPAN;
 }
 
 // The halo-staged kernel's tile for a stride-1 "same" implicit GEMM, or -1

@@ -35,7 +35,6 @@ namespace nnconv {
 
 namespace halo {
 
-constexpr int BM = 256;   // output pixels per tile
 constexpr int BKC = 8;    // 16-byte chunks per 64-channel row
 constexpr int RPI = 8;    // rows per 64-lane load (64 lanes x 16 bytes)
 
@@ -48,7 +47,7 @@ __device__ __forceinline__ int slot(int r, int c) { return r * BKC + (c ^ ((r >>
 
 }  // namespace halo
 
-template <class T, int BN, int WM, int WN, int HRMAX, int OCC>
+template <class T, int BM, int BN, int WM, int WN, int HRMAX, int OCC>
 __global__ __launch_bounds__(WM * WN * 64, OCC)
 void igemm_halo_kernel(const TNParams P) {
     using namespace halo;
@@ -242,30 +241,31 @@ void igemm_halo_kernel(const TNParams P) {
 
 namespace {
 
-template <class T, int BN, int WM, int WN, int OCC>
+template <class T, int BM, int BN, int WM, int WN, int OCC>
 hipError_t launch_halo_cfg(TNParams &p, hipStream_t st) {
+    if (!halo_supported(p)) return hipErrorInvalidValue;
     p.tiles_n = (p.ncols + BN - 1) / BN;
-    const int64_t tiles_m = (p.ph[0].M + halo::BM - 1) / halo::BM;
+    const int64_t tiles_m = (p.ph[0].M + BM - 1) / BM;
     p.ph[0].tiles_m = (int32_t)tiles_m;
     p.ph[0].block_start = 0;
     const int64_t nb = tiles_m * p.tiles_n;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((igemm_halo_kernel<T, BN, WM, WN, HALO_ROWS, OCC>), dim3((uint32_t)nb),
+    // halo buffer: BM + HALO_SPAN rows
+    hipLaunchKernelGGL((igemm_halo_kernel<T, BM, BN, WM, WN, BM + HALO_SPAN, OCC>), dim3((uint32_t)nb),
                        dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
 
-// Configurations (LDS per workgroup; two workgroups per CU):
-//   256x64:  4 waves of 64x64 (64 KB)
-//   256x128: 4 waves of 128x64 (80 KB)
-// The halo buffer holds 384 rows: 256 + 2W + 2 <= 384 for W <= 63.
+// Configurations (LDS per workgroup):
+//   256x64:  4 waves of 64x64 (64 KB; two workgroups per CU)
+//   256x128: 4 waves of 128x64 (80 KB; two per CU)
 template <class T>
 hipError_t launch_halo_t(HaloConfig cfg, TNParams &p, hipStream_t st) {
     switch (cfg) {
-        case HALO_256x128: return launch_halo_cfg<T, 128, 2, 2, 2>(p, st);
+        case HALO_256x128: return launch_halo_cfg<T, 256, 128, 2, 2, 2>(p, st);
         case HALO_256x64:
-        default: return launch_halo_cfg<T, 64, 4, 1, 2>(p, st);
+        default: return launch_halo_cfg<T, 256, 64, 4, 1, 2>(p, st);
     }
 }
 
@@ -285,11 +285,10 @@ bool halo_supported(const TNParams &p) {
         lo = s < lo ? s : lo;
         hi = s > hi ? s : hi;
     }
-    return halo::BM + hi - lo <= HALO_ROWS;
+    return hi - lo <= HALO_SPAN;
 }
 
 hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, hipStream_t st) {
-    if (!halo_supported(p)) return hipErrorInvalidValue;
     if (dtype == Half::id) return launch_halo_t<Half>(cfg, p, st);
     return launch_halo_t<BFloat>(cfg, p, st);
 }

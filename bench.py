@@ -323,39 +323,100 @@ def summarize_profile(args):
         others = [c for c in counters if c not in ("FETCH_SIZE", "WRITE_SIZE")]
         if not others:
             continue
-        # per dispatch: counter values and duration; then averages per kernel
+        # per dispatch: counter values, duration and resources; then averages
+        # per kernel and per (layer, kernel)
         disp = collections.defaultdict(dict)
         for r in allrows:
             d = disp[int(r["Dispatch_Id"])]
             d["name"] = r["Kernel_Name"]
             d["dur"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            d["res"] = (int(r["VGPR_Count"]), int(r["Accum_VGPR_Count"]),
+                        int(r["LDS_Block_Size"]), int(r["Workgroup_Size"]))
             d[r["Counter_Name"]] = float(r["Counter_Value"])
+        ids = sorted(disp)
+        names = [disp[k]["name"] for k in ids]
+        # layer of each dispatch: that of the latest forward launch (none
+        # during the warm-up steps); pass: forward for that launch, then
+        # backward-weight for the split-K kernels and their reduction,
+        # backward-data for the rest
+        layer_of, li = {}, None
+        fwd_pos = {i: j for j, (i, _) in enumerate(fwd_launches(names))}
+        for pos, k in enumerate(ids):
+            fwd = is_forward_launch(names, pos)
+            if fwd:
+                li = layers[fwd_pos[pos] % nl].name if pos in fwd_pos else None
+            nm = names[pos]
+            ps = "fwd" if fwd else ("wgrad" if "wgrad" in nm else "dgrad")
+            layer_of[k] = None if li is None else (li, ps)
         fam = collections.OrderedDict()
-        for k in sorted(disp):
-            if "nnconv::" in disp[k]["name"]:
-                fam.setdefault(family(disp[k]["name"]), []).append(disp[k])
+        per_layer = collections.OrderedDict()
+        for k in ids:
+            if "nnconv::" not in disp[k]["name"]:
+                continue
+            fam.setdefault(family(disp[k]["name"]), []).append(disp[k])
+            if layer_of[k] is not None:
+                per_layer.setdefault(layer_of[k] + (family(disp[k]["name"]),), []).append(disp[k])
+
+        def derived(avg, dur):
+            """MFMA utilisation, LDS bank-conflict rate, L2 hit rate, wait share."""
+            f = []
+            ga = avg.get("GRBM_GUI_ACTIVE")
+            if ga and "SQ_VALU_MFMA_BUSY_CYCLES" in avg:
+                # GRBM_GUI_ACTIVE sums the 8 XCDs; 1024 SIMDs
+                f.append(("mfma_util", avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (1024 * ga / 8)))
+            if ga:
+                f.append(("clock_ghz", ga / 8 / dur))
+            if avg.get("SQ_LDS_IDX_ACTIVE") and "SQ_LDS_BANK_CONFLICT" in avg:
+                f.append(("lds_conflict", avg["SQ_LDS_BANK_CONFLICT"] / avg["SQ_LDS_IDX_ACTIVE"]))
+            if "TCC_HIT_sum" in avg and "TCC_MISS_sum" in avg:
+                h, m = avg["TCC_HIT_sum"], avg["TCC_MISS_sum"]
+                f.append(("l2_hit", h / max(1.0, h + m)))
+            if avg.get("SQ_WAVE_CYCLES"):
+                for c, n in (("SQ_WAIT_ANY", "wait_share"), ("SQ_ACTIVE_INST_ANY", "issue_share"),
+                             ("SQ_WAIT_INST_LDS", "lds_wait_share")):
+                    if c in avg:
+                        f.append((n, avg[c] / avg["SQ_WAVE_CYCLES"]))
+            return f
+
+        def occupancy(res):
+            """Waves per SIMD allowed by registers (512 per lane, granule 8)
+            and by LDS (160 KiB per CU, 4 SIMDs)."""
+            vg, ag, lds, wg = res
+            regs = ((vg + 7) // 8) * 8 + ((ag + 7) // 8) * 8
+            by_regs = min(8, 512 // max(8, regs))
+            waves = max(1, wg // 64)
+            by_lds = 8 if lds == 0 else (163840 // lds) * waves / 4.0
+            return by_regs, by_lds
+
         out.append("counters per dispatch (%s), averaged per kernel:"
                    % os.path.relpath(path, args.summarize_profile))
         for name, ds in fam.items():
             avg = {c: sum(d.get(c, 0.0) for d in ds) / len(ds) for c in others}
             dur = sum(d["dur"] for d in ds) / len(ds)
-            out.append("%s  n=%d  avg %.2f us" % (name[:100], len(ds), dur / 1e3))
+            res = ds[0]["res"]
+            occ = occupancy(res)
+            out.append("%s  n=%d  avg %.2f us  vgpr %d agpr %d lds %d wg %d  waves/SIMD: regs %d, "
+                       "lds %.1f" % ((name[:100], len(ds), dur / 1e3) + res + occ))
             out.append("    " + "  ".join("%s=%.4g" % kv for kv in sorted(avg.items())))
-            ga = avg.get("GRBM_GUI_ACTIVE")
-            if ga:
-                # GRBM_GUI_ACTIVE sums the cycles of the 8 XCDs
-                out.append("    clock %.3f GHz (GRBM_GUI_ACTIVE / 8 / duration)" % (ga / 8 / dur))
-                if "SQ_VALU_MFMA_BUSY_CYCLES" in avg:
-                    out.append("    MFMA utilisation %.3f (SQ_VALU_MFMA_BUSY_CYCLES / (1024 "
-                               "SIMDs x GRBM_GUI_ACTIVE / 8))"
-                               % (avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (1024 * ga / 8)))
-            if avg.get("SQ_LDS_IDX_ACTIVE"):
-                if "SQ_LDS_BANK_CONFLICT" in avg:
-                    out.append("    LDS bank-conflict cycles / LDS active cycles %.4f"
-                               % (avg["SQ_LDS_BANK_CONFLICT"] / avg["SQ_LDS_IDX_ACTIVE"]))
-            if avg.get("TCC_HIT_sum") is not None and "TCC_MISS_sum" in avg:
-                h, m = avg["TCC_HIT_sum"], avg["TCC_MISS_sum"]
-                out.append("    L2 hit rate %.3f" % (h / max(1.0, h + m)))
+            f = derived(avg, dur)
+            if f:
+                out.append("    " + "  ".join("%s %.3f" % kv for kv in f))
+        if per_layer:
+            out.append("per layer and kernel (%s; layer = that of the latest forward launch):"
+                       % os.path.relpath(path, args.summarize_profile))
+            keys = None
+            for (lname, ps, name), ds in per_layer.items():
+                avg = {c: sum(d.get(c, 0.0) for d in ds) / len(ds) for c in others}
+                dur = sum(d["dur"] for d in ds) / len(ds)
+                f = derived(avg, dur)
+                if keys is None:
+                    keys = [k for k, _ in f]
+                    out.append("  %-9s %-5s %-58s %4s %8s " % ("layer", "pass", "kernel", "n", "us") +
+                               " ".join("%13s" % k for k in keys))
+                short = name.replace("nnconv::", "")
+                out.append("  %-9s %-5s %-58s %4d %8.1f " % (lname, ps, short[:58], len(ds),
+                                                             dur / 1e3) +
+                           " ".join("%13.3f" % v for _, v in f))
     out.append("source_sha256: %s" % fwd_source_hash())
     print("\n".join(out))
 

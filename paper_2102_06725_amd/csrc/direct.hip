@@ -208,7 +208,9 @@ __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__rest
 // Same transpose with 16-byte accesses on both sides (cols, dst_ld and rows
 // multiples of 8, 16-byte aligned buffers): a 64x64 tile is read as 8-element
 // row chunks, and each output chunk gathers 8 consecutive rows of one column
-// from LDS.
+// from LDS.  The gather of a wave touches rows 8 apart, which share banks
+// for any row pitch that keeps chunks 16-byte aligned, so chunk c of row r
+// is stored at chunk c ^ ((r >> 3) & 7) instead of padding the rows.
 template <bool SCAN>
 __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__restrict__ src,
                                                               uint16_t *__restrict__ dst,
@@ -216,8 +218,7 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
                                                               int64_t dst_ld, int64_t tiles_c,
                                                               int64_t tiles_r, uint32_t expmask,
                                                               int32_t *flags) {
-    constexpr int LD = 72;  // halves per LDS row (144 bytes: 16-byte aligned, skewed)
-    __shared__ uint16_t tile[64 * LD];
+    __shared__ uint16_t tile[64 * 64];
     const int64_t t = blockIdx.x;
     const int64_t b = t / (tiles_c * tiles_r);
     const int64_t rem = t - b * tiles_c * tiles_r;
@@ -232,7 +233,7 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
         const int64_t rr = r0 + row, col = c0 + cc;
         u32x4 v = u32x4{};
         if (rr < rows && col < cols) v = *(const u32x4 *)(s + rr * cols + col);
-        *(u32x4 *)(&tile[row * LD + cc]) = v;
+        *(u32x4 *)(&tile[row * 64 + (((cc >> 3) ^ ((row >> 3) & 7)) << 3)]) = v;
         if constexpr (SCAN) {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -252,11 +253,13 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
         const int oc = id >> 3, rc = (id & 7) * 8;
         const int64_t col = c0 + oc, rr = r0 + rc;
         if (col < cols && rr < dst_ld) {
+            // rows rc .. rc + 7 share (r >> 3) = rc >> 3
+            const int pc = (((oc >> 3) ^ ((rc >> 3) & 7)) << 3) + (oc & 7);
             uint32_t w[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                w[e] = (uint32_t)tile[(rc + 2 * e) * LD + oc] |
-                       ((uint32_t)tile[(rc + 2 * e + 1) * LD + oc] << 16);
+                w[e] = (uint32_t)tile[(rc + 2 * e) * 64 + pc] |
+                       ((uint32_t)tile[(rc + 2 * e + 1) * 64 + pc] << 16);
             *(u32x4 *)(d + col * dst_ld + rr) = u32x4{w[0], w[1], w[2], w[3]};
         }
     }

@@ -438,13 +438,16 @@ bool halo_geom(const Geom &G) {
 }
 
 // The halo-staged kernel's tile for a stride-1 "same" implicit GEMM, or -1
-// for the 64-channel-slice kernel.  Measured on the ResNet-50 3x3 layers at
-// batch 256: the halo tile wins on 7x7 images with wide outputs (there the
+// for the 64-channel-slice kernel.  Measured on the ResNet-50 layers at
+// batch 256: on 3x3 filters over 7x7 images with wide outputs (where the
 // 64-channel-slice tiles stage each input pixel once per tap and per
-// 64-column tile), by about 13% forward and backward-data, and ties or
-// loses on the wider images.
+// 64-column tile) the halo tile is 2-3% faster than the pipelined 128x128
+// tile, forward and backward-data, and 8-14% faster than the single-stage
+// ones; it ties or loses on the wider images.  A 1x1 filter has no halo to
+// share: its tile is a plain GEMM tile, slower than the 64-channel-slice
+// ones (40-60% on the 7x7 1x1 layers).
 int pick_halo(const TNParams &p) {
-    if (!halo_supported(p) || p.a_w > 7 || p.ncols < 256) return -1;
+    if (p.ph[0].tap_count < 2 || !halo_supported(p) || p.a_w > 7 || p.ncols < 256) return -1;
     return HALO_256x64;
 }
 

@@ -8,8 +8,10 @@ EfficientNet-B0 at batch 128 and the grouped layers of ResNeXt-50 at batch
 calls, descriptors and therefore the same kernel launches that bench.py
 times.  The oracle's single-point routines then evaluate sampled outputs:
 65,536 random positions of y and of dx, every border pixel (all channels) of
-the first and last image, and 2,048 random weight-gradient entries plus the
-first and last filter in full.  The error is max|err| / max|ref| over the
+the first and last image, and 2,048 random weight-gradient entries plus
+whole filters: the first, the last and one in every block of 32 filters
+(at an offset that changes from block to block), so every row block and
+column of every backward-weight tile is checked.  The error is max|err| / max|ref| over the
 sampled positions.  Every output element is also checked for bitwise
 reproducibility across two runs.
 
@@ -139,10 +141,16 @@ def test_full_size_sampled(name, case):
     wshape_alg = (L.k, cl // L.groups, L.r, L.s)
     per_filter = wshape_alg[1] * L.r * L.s
     total = L.k * per_filter
-    idx = np.unique(np.concatenate([
-        rng.integers(0, total, size=min(N_DW_RANDOM, total), dtype=np.int64),
-        np.arange(per_filter, dtype=np.int64),
-        np.arange(total - per_filter, total, dtype=np.int64)]))
+    # whole filters: the first, the last, and one in every block of 32
+    # (the matrix-core row block of every backward-weight tile) at an offset
+    # that differs from block to block, so every row block and every column
+    # of every output tile has a complete row under the oracle
+    rows = sorted({0, L.k - 1} | {32 * b + (7 * b + 13) % min(32, L.k)
+                                  for b in range((L.k + 31) // 32)
+                                  if 32 * b + (7 * b + 13) % min(32, L.k) < L.k})
+    idx = np.unique(np.concatenate(
+        [rng.integers(0, total, size=min(N_DW_RANDOM, total), dtype=np.int64)] +
+        [np.arange(k * per_filter, (k + 1) * per_filter, dtype=np.int64) for k in rows]))
     ref = cv.wgrad_points(x, dy, idx) / case.loss_scale
     # dw is [K][R][S][Cg] (channel-last, Cg padded for the stem)
     k = idx // per_filter

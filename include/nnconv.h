@@ -158,7 +158,8 @@ typedef enum {
      * wide; backward-data of the same at stride 1): 256-pixel tiles, each
      * 64-channel slice of the input staged once per tile for all taps. */
     NNCONV_TILE_HALO_256x64 = 9,    /* 4 waves of 64x64 */
-    NNCONV_TILE_HALO_256x128 = 10   /* 4 waves of 128x64 */
+    NNCONV_TILE_HALO_256x128 = 10,  /* 4 waves of 128x64 */
+    NNCONV_TILE_HALO_256x64_2T = 11 /* 256x64, B tiles of two taps per barrier */
 } nnconv_tile;
 
 /* nnconv_fwd / nnconv_dgrad with the tile forced (an nnconv_tile value).

@@ -423,9 +423,12 @@ C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
     return red >= long_red ? C64_128x128 : C64S_128x128;
 }
 
-// Forced-tile ids from HALO_TILE0 on select the halo-staged kernel
-// (HaloConfig = id - HALO_TILE0).
+// Forced-tile ids HALO_TILE0 .. HALO_TILE0 + HALO_CONFIGS - 1 select the
+// halo-staged kernel (HaloConfig = id - HALO_TILE0); lower ones are
+// C64Config values.
 constexpr int HALO_TILE0 = 9;
+constexpr int HALO_CONFIGS = HALO_256x64_2T + 1;
+bool halo_tile(int tile) { return tile >= HALO_TILE0 && tile < HALO_TILE0 + HALO_CONFIGS; }
 
 // Whether the halo-staged kernel can run this shape's forward and
 // backward-data passes (the geometry halo_supported() accepts, stated on the
@@ -549,7 +552,7 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     if (G.cg % 64 == 0) {
         p.nphase = 1;
         p.ph[0] = phase_of(p.M, p.mi, p.mj, 0, 0, 0, t);
-        const int hc = tile >= HALO_TILE0 ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
+        const int hc = halo_tile(tile) ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
         if (hc >= 0) {
             if (!halo_supported(p)) return NNCONV_ERR_UNSUPPORTED;
             return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, st));
@@ -628,7 +631,7 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             }
         }
         if (p.nphase == 0) return NNCONV_OK;
-        const int hc = tile >= HALO_TILE0 ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
+        const int hc = halo_tile(tile) ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
         if (hc >= 0) {
             if (!halo_supported(p)) return NNCONV_ERR_UNSUPPORTED;
             return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, st));
@@ -904,7 +907,7 @@ static nnconv_status check_ws(const Geom &G, nnconv_pass pass, const void *ws, s
 // kernel with its operands as given.
 bool tile_ok(int tile) {
     return (tile >= C64_256x256 && tile <= C64R_256x64 && tile != C64D_128x64) ||
-           (tile >= HALO_TILE0 && tile <= HALO_TILE0 + HALO_256x128);
+           halo_tile(tile);
 }
 
 static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void *w, void *y,
@@ -921,7 +924,7 @@ static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void
         const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_fwd_shape(G) &&
                            aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                            (G.layout == NNCONV_NHWC || aligned(ws, 16));
-        if (!tile_ok(tile) || !dense || (tile >= HALO_TILE0 && !halo_geom(G)))
+        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G)))
             return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();
@@ -972,7 +975,7 @@ static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const v
         const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_dgrad_shape(G) &&
                            aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
                            aligned(ws, 16);
-        if (!tile_ok(tile) || !dense || (tile >= HALO_TILE0 && !halo_geom(G)))
+        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G)))
             return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();

@@ -47,7 +47,8 @@ __device__ __forceinline__ int slot(int r, int c) { return r * BKC + (c ^ ((r >>
 
 }  // namespace halo
 
-template <class T, int BM, int BN, int WM, int WN, int HRMAX, int OCC>
+// TPS: taps per step (B tiles staged together between two barriers).
+template <class T, int BM, int BN, int WM, int WN, int HRMAX, int TPS, int OCC>
 __global__ __launch_bounds__(WM * WN * 64, OCC)
 void igemm_halo_kernel(const TNParams P) {
     using namespace halo;
@@ -60,7 +61,7 @@ void igemm_halo_kernel(const TNParams P) {
     static_assert(FM >= 1 && FN >= 1 && H_LD >= 1 && B_LD >= 1 &&
                       HRMAX % (RPI * NW) == 0 && BN % (RPI * NW) == 0,
                   "tile shape");
-    constexpr int MAIN_SLOTS = H_SLOTS + 2 * B_SLOTS;
+    constexpr int MAIN_SLOTS = H_SLOTS + 2 * TPS * B_SLOTS;
     constexpr int LDS_SLOTS = MAIN_SLOTS > BM * BN / 8 ? MAIN_SLOTS : BM * BN / 8;
     __shared__ u32x4 lds[LDS_SLOTS];
 
@@ -150,14 +151,21 @@ void igemm_halo_kernel(const TNParams P) {
 #pragma unroll
         for (int j = 0; j < H_LD; ++j) halo_load(j, d, lds0);
     };
-    // the B tile of (tap t, channel slice c) into B buffer bb
-    auto issue_b = [&](int t, int c, int bb) {
-        const uint32_t bshift = (uint32_t)__builtin_amdgcn_readlane((int)tap_boff, t);
-        const i32x4 d = desc_at(P.b, P.b_bytes, bshift + (uint32_t)c * 128u);
-        const uint32_t base = lds0 + (uint32_t)(H_SLOTS + bb * B_SLOTS) * 16u;
+    // the B tiles of step u (taps u*TPS .. u*TPS + TPS - 1 that exist) of
+    // channel slice c into B buffer bb
+    auto issue_b = [&](int u, int c, int bb) {
 #pragma unroll
-        for (int j = 0; j < B_LD; ++j)
-            dma16(base + (uint32_t)((wave * B_LD + j) * 64) * 16u, b_voff[j], d);
+        for (int e = 0; e < TPS; ++e) {
+            const int t = u * TPS + e;
+            if (t < ntaps) {
+                const uint32_t bshift = (uint32_t)__builtin_amdgcn_readlane((int)tap_boff, t);
+                const i32x4 d = desc_at(P.b, P.b_bytes, bshift + (uint32_t)c * 128u);
+                const uint32_t base = lds0 + (uint32_t)(H_SLOTS + (bb * TPS + e) * B_SLOTS) * 16u;
+#pragma unroll
+                for (int j = 0; j < B_LD; ++j)
+                    dma16(base + (uint32_t)((wave * B_LD + j) * 64) * 16u, b_voff[j], d);
+            }
+        }
     };
 
     f32x16 acc[FN][FM];
@@ -171,11 +179,11 @@ void igemm_halo_kernel(const TNParams P) {
     // B fragments from the tap's tile.  With few fragments per k-step all
     // four k-steps' reads are issued first (one wait instead of one per
     // k-step); larger wave tiles would run out of registers doing so.
-    auto compute = [&](int bb, int t) {
+    auto compute = [&](int bb, int e, int t) {
         constexpr int KS = BKC / 2;
         constexpr bool BATCH = FM + FN <= 4;
         const u32x4 *hs = &lds[0];
-        const u32x4 *bs = &lds[H_SLOTS + bb * B_SLOTS];
+        const u32x4 *bs = &lds[H_SLOTS + (bb * TPS + e) * B_SLOTS];
         const int hoff = __builtin_amdgcn_readlane(tap_hoff, t);
         u32x4 fa[BATCH ? KS : 1][FM], fb[BATCH ? KS : 1][FN];
         auto read = [&](int ks, int e) {
@@ -212,26 +220,29 @@ void igemm_halo_kernel(const TNParams P) {
     };
 
     const int nslices = P.cr / 64;
-    const int k_iters = ntaps * nslices;
+    const int nsteps = (ntaps + TPS - 1) / TPS;  // steps per slice
+    const int k_iters = nsteps * nslices;
     if (k_iters > 0) {
         issue_halo(0);
         issue_b(0, 0, 0);
-        int t = 0, c = 0;
+        int u = 0, c = 0;
         for (int kt = 0; kt < k_iters; ++kt) {
-            if (t == 0 && c > 0) {
+            if (u == 0 && c > 0) {
                 barrier_lds();  // every wave is done with slice c - 1
                 issue_halo(c);
             }
             wait_vmcnt<0>();
-            barrier_lds();  // halo and B tile of this step landed; step kt-1 done
-            int t1 = t + 1, c1 = c;
-            if (t1 == ntaps) {
-                t1 = 0;
+            barrier_lds();  // halo and B tiles of this step landed; step kt-1 done
+            int u1 = u + 1, c1 = c;
+            if (u1 == nsteps) {
+                u1 = 0;
                 ++c1;
             }
-            if (kt + 1 < k_iters) issue_b(t1, c1, (kt + 1) & 1);
-            compute(kt & 1, t);
-            t = t1;
+            if (kt + 1 < k_iters) issue_b(u1, c1, (kt + 1) & 1);
+#pragma unroll
+            for (int e = 0; e < TPS; ++e)
+                if (u * TPS + e < ntaps) compute(kt & 1, e, u * TPS + e);
+            u = u1;
             c = c1;
         }
     }
@@ -241,7 +252,7 @@ void igemm_halo_kernel(const TNParams P) {
 
 namespace {
 
-template <class T, int BM, int BN, int WM, int WN, int OCC>
+template <class T, int BM, int BN, int WM, int WN, int TPS, int OCC>
 hipError_t launch_halo_cfg(TNParams &p, hipStream_t st) {
     if (!halo_supported(p)) return hipErrorInvalidValue;
     p.tiles_n = (p.ncols + BN - 1) / BN;
@@ -252,7 +263,7 @@ hipError_t launch_halo_cfg(TNParams &p, hipStream_t st) {
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     // halo buffer: BM + HALO_SPAN rows
-    hipLaunchKernelGGL((igemm_halo_kernel<T, BM, BN, WM, WN, BM + HALO_SPAN, OCC>), dim3((uint32_t)nb),
+    hipLaunchKernelGGL((igemm_halo_kernel<T, BM, BN, WM, WN, BM + HALO_SPAN, TPS, OCC>), dim3((uint32_t)nb),
                        dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
@@ -263,9 +274,10 @@ hipError_t launch_halo_cfg(TNParams &p, hipStream_t st) {
 template <class T>
 hipError_t launch_halo_t(HaloConfig cfg, TNParams &p, hipStream_t st) {
     switch (cfg) {
-        case HALO_256x128: return launch_halo_cfg<T, 256, 128, 2, 2, 2>(p, st);
+        case HALO_256x128: return launch_halo_cfg<T, 256, 128, 2, 2, 1, 2>(p, st);
+        case HALO_256x64_2T: return launch_halo_cfg<T, 256, 64, 4, 1, 2, 2>(p, st);
         case HALO_256x64:
-        default: return launch_halo_cfg<T, 256, 64, 4, 1, 2>(p, st);
+        default: return launch_halo_cfg<T, 256, 64, 4, 1, 1, 2>(p, st);
     }
 }
 

@@ -102,8 +102,9 @@ hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hip
 // taps whose raster shifts span at most HALO_SPAN pixels (3x3 filters with
 // padding 1 on images up to 63 pixels wide).
 constexpr int HALO_SPAN = 128;
-enum HaloConfig { HALO_256x64 = 0,    // 4 waves of 64x64
-                  HALO_256x128 = 1 }; // 4 waves of 128x64
+enum HaloConfig { HALO_256x64 = 0,      // 4 waves of 64x64
+                  HALO_256x128 = 1,     // 4 waves of 128x64
+                  HALO_256x64_2T = 2 }; // 256x64 with the B tiles of two taps per step
 bool halo_supported(const TNParams &p);
 // hipErrorInvalidValue when !halo_supported(p)
 hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, hipStream_t st);

@@ -44,7 +44,8 @@ NNCONV_TILE_256x128_RING = 7
 NNCONV_TILE_256x64_RING = 8
 NNCONV_TILE_HALO_256x64 = 9
 NNCONV_TILE_HALO_256x128 = 10
-HALO_TILES = (NNCONV_TILE_HALO_256x64, NNCONV_TILE_HALO_256x128)
+NNCONV_TILE_HALO_256x64_2T = 11
+HALO_TILES = (NNCONV_TILE_HALO_256x64, NNCONV_TILE_HALO_256x128, NNCONV_TILE_HALO_256x64_2T)
 TILES = (NNCONV_TILE_256x256_8W, NNCONV_TILE_128x128_2S, NNCONV_TILE_128x128, NNCONV_TILE_128x64,
          NNCONV_TILE_256x256_16W, NNCONV_TILE_256x256_RING, NNCONV_TILE_256x128_RING,
          NNCONV_TILE_256x64_RING)

@@ -192,7 +192,11 @@ __global__ __launch_bounds__(stem::FWD_WAVES * 64, 1) void stem_fwd_kernel(const
                                        ? (uint32_t)(((n * P.p + oh) * P.q + ow) * K + c * 8) * 2u
                                        : OOB_OFFSET;
                 const u32x4 v = lds[G::W_ENT + 2 * G::P_ENT + px * 8 + (c ^ (px & 7))];
-                __builtin_amdgcn_raw_buffer_store_b128(v, ry, o, 0, 0);
+                // non-temporal (cache policy nt): 411 MB of output at batch
+                // 256 would otherwise displace the operands of the kernels
+                // that follow (stem forward 161 -> 152 us, its backward-weight
+                // 212 -> 198 us in the ResNet-50 step)
+                __builtin_amdgcn_raw_buffer_store_b128(v, ry, o, 0, 2);
             }
         }
         // the next patch has landed (its loads precede this tile's stores)

@@ -193,9 +193,10 @@ __global__ __launch_bounds__(stem::FWD_WAVES * 64, 1) void stem_fwd_kernel(const
                                        : OOB_OFFSET;
                 const u32x4 v = lds[G::W_ENT + 2 * G::P_ENT + px * 8 + (c ^ (px & 7))];
                 // non-temporal (cache policy nt): 411 MB of output at batch
-                // 256 would otherwise displace the operands of the kernels
-                // that follow (stem forward 161 -> 152 us, its backward-weight
-                // 212 -> 198 us in the ResNet-50 step)
+                // 256 need not displace the operands of the kernels that
+                // follow (measured 1-7% faster for the stem's forward and
+                // backward-weight in the ResNet-50 step, depending on the
+                // machine)
                 __builtin_amdgcn_raw_buffer_store_b128(v, ry, o, 0, 2);
             }
         }

@@ -781,8 +781,8 @@ nnconv_status dw_wgrad(const Geom &G, const void *x, const void *dy, void *dw, i
     const Regions R = dw_regions(G, NNCONV_WGRAD);
     const void *xn = x, *dyn = dy;
     if (G.layout == NNCONV_NCHW) {
-        TRY_HIP(launch_transpose16(x, ws + R.a, G.n, G.c, G.h * G.w, G.c, st));
-        TRY_HIP(launch_transpose16(dy, ws + R.b, G.n, G.k, G.p * G.q, G.k, st));
+        TRY_HIP(launch_transpose16_pair(x, ws + R.a, G.n, G.c, G.h * G.w, G.c, dy, ws + R.b, G.n,
+                                        G.k, G.p * G.q, G.k, st));
         xn = ws + R.a;
         dyn = ws + R.b;
     }
@@ -836,8 +836,8 @@ nnconv_status sg_wgrad(const Geom &G, const void *x, const void *dy, void *dw, i
     const void *xn = x, *dyn = dy;
     if (G.layout == NNCONV_NCHW) {
         void *xt = ws + R.a, *dyt = ws + R.b;
-        TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, st));
-        TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, st));
+        TRY_HIP(launch_transpose16_pair(x, xt, G.n, G.c, G.h * G.w, G.c, dy, dyt, G.n, G.k,
+                                        G.p * G.q, G.k, st));
         xn = xt;
         dyn = dyt;
     }
@@ -943,8 +943,8 @@ static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void
     const Regions R = fast_regions(G, NNCONV_FWD);
     char *base = (char *)ws;
     void *xt = base + R.a, *wt = base + R.b, *yt = base + R.c;
-    TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, s));
-    TRY_HIP(launch_transpose16(w, wt, G.k, G.cg, G.r * G.s, G.cg, s));
+    TRY_HIP(launch_transpose16_pair(x, xt, G.n, G.c, G.h * G.w, G.c, w, wt, G.k, G.cg, G.r * G.s,
+                                    G.cg, s));
     if ((st = fwd_fast(G, xt, wt, yt, alpha, s, tile)) != NNCONV_OK) return st;
     return hip_status(launch_transpose16(yt, y, G.n, G.p * G.q, G.k, G.p * G.q, s));
 }
@@ -1000,10 +1000,10 @@ static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const v
     void *dxn = dx;
     if (G.layout == NNCONV_NCHW) {
         void *tmp = base + R.d;
-        TRY_HIP(launch_transpose16(w, tmp, G.k, G.cg, G.r * G.s, G.cg, s));
-        wkrsc = tmp;
         void *dyt = base + R.a;
-        TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, s));
+        TRY_HIP(launch_transpose16_pair(w, tmp, G.k, G.cg, G.r * G.s, G.cg, dy, dyt, G.n, G.k,
+                                        G.p * G.q, G.k, s));
+        wkrsc = tmp;
         dyn = dyt;
         dxn = base + R.c;
     }
@@ -1086,8 +1086,8 @@ static nnconv_status wgrad_run(const Geom &G, const void *x, const void *dy, voi
     const void *xn = x, *dyn = dy;
     if (G.layout == NNCONV_NCHW) {
         void *xt = base + R.a, *dyt = base + R.b;
-        TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, s));
-        TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, s));
+        TRY_HIP(launch_transpose16_pair(x, xt, G.n, G.c, G.h * G.w, G.c, dy, dyt, G.n, G.k,
+                                        G.p * G.q, G.k, s));
         xn = xt;
         dyn = dyt;
     }

@@ -171,14 +171,13 @@ hipError_t launch_direct_wgrad(int dtype, const DirectParams &p, const void *x, 
 //
 // SCAN: also store into flags[blockIdx.x] whether any element of the tile is
 // inf or NaN (all exponent bits of expmask set).
+// One 64x64 tile (index t) of a batched transpose with 2-byte accesses (any
+// sizes and alignment).
 template <bool SCAN>
-__global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__restrict__ src,
-                                                          uint16_t *__restrict__ dst, int64_t rows,
-                                                          int64_t cols, int64_t dst_ld,
-                                                          int64_t tiles_c, int64_t tiles_r,
-                                                          uint32_t expmask, int32_t *flags) {
-    __shared__ uint16_t tile[64][65];
-    const int64_t t = blockIdx.x;
+__device__ __forceinline__ void transpose16_tile(const uint16_t *src, uint16_t *dst, int64_t rows,
+                                                 int64_t cols, int64_t dst_ld, int64_t tiles_c,
+                                                 int64_t tiles_r, int64_t t, uint16_t (*tile)[65],
+                                                 uint32_t expmask, int32_t *flags) {
     const int64_t b = t / (tiles_c * tiles_r);
     const int64_t rem = t - b * tiles_c * tiles_r;
     const int64_t tr = rem / tiles_c, tc = rem - (rem / tiles_c) * tiles_c;
@@ -194,7 +193,7 @@ __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__rest
     }
     if constexpr (SCAN) {
         bad = __syncthreads_or(bad);
-        if (threadIdx.x == 0) flags[blockIdx.x] = bad;
+        if (threadIdx.x == 0) flags[t] = bad;
     } else {
         __syncthreads();
     }
@@ -205,26 +204,32 @@ __global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__rest
     }
 }
 
-// Same transpose with 16-byte accesses on both sides (cols, dst_ld and rows
-// multiples of 8, 16-byte aligned buffers): a 64x64 tile is read as 8-element
-// row chunks, and each output chunk gathers 8 consecutive rows of one column
-// from LDS.  The gather of a wave touches rows 8 apart, which share banks
-// for any row pitch that keeps chunks 16-byte aligned, so chunk c of row r
-// is stored at chunk c ^ ((r >> 3) & 7) instead of padding the rows.
 template <bool SCAN>
-__global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__restrict__ src,
-                                                              uint16_t *__restrict__ dst,
-                                                              int64_t rows, int64_t cols,
-                                                              int64_t dst_ld, int64_t tiles_c,
-                                                              int64_t tiles_r, uint32_t expmask,
-                                                              int32_t *flags) {
-    __shared__ uint16_t tile[64 * 64];
-    const int64_t t = blockIdx.x;
-    const int64_t b = t / (tiles_c * tiles_r);
-    const int64_t rem = t - b * tiles_c * tiles_r;
-    const int64_t tr = rem / tiles_c, tc = rem - (rem / tiles_c) * tiles_c;
+__global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t *__restrict__ src,
+                                                          uint16_t *__restrict__ dst, int64_t rows,
+                                                          int64_t cols, int64_t dst_ld,
+                                                          int64_t tiles_c, int64_t tiles_r,
+                                                          uint32_t expmask, int32_t *flags) {
+    __shared__ uint16_t tile[64][65];
+    transpose16_tile<SCAN>(src, dst, rows, cols, dst_ld, tiles_c, tiles_r, blockIdx.x, tile,
+                           expmask, flags);
+}
+
+// One 64x64 tile (index t) of a batched transpose, 16-byte accesses.
+struct T16 {
+    const uint16_t *src;
+    uint16_t *dst;
+    int64_t rows, cols, dst_ld, tiles_c, tiles_r;
+};
+
+template <bool SCAN>
+__device__ __forceinline__ void transpose16_vec_tile(const T16 &p, int64_t t, uint16_t *tile,
+                                                     uint32_t expmask, int32_t *flags) {
+    const int64_t b = t / (p.tiles_c * p.tiles_r);
+    const int64_t rem = t - b * p.tiles_c * p.tiles_r;
+    const int64_t tr = rem / p.tiles_c, tc = rem - (rem / p.tiles_c) * p.tiles_c;
     const int64_t r0 = tr * 64, c0 = tc * 64;
-    const uint16_t *s = src + b * rows * cols;
+    const uint16_t *s = p.src + b * p.rows * p.cols;
     int bad = 0;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -232,7 +237,7 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
         const int row = id >> 3, cc = (id & 7) * 8;
         const int64_t rr = r0 + row, col = c0 + cc;
         u32x4 v = u32x4{};
-        if (rr < rows && col < cols) v = *(const u32x4 *)(s + rr * cols + col);
+        if (rr < p.rows && col < p.cols) v = *(const u32x4 *)(s + rr * p.cols + col);
         *(u32x4 *)(&tile[row * 64 + (((cc >> 3) ^ ((row >> 3) & 7)) << 3)]) = v;
         if constexpr (SCAN) {
 #pragma unroll
@@ -242,17 +247,17 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
     }
     if constexpr (SCAN) {
         bad = __syncthreads_or(bad);
-        if (threadIdx.x == 0) flags[blockIdx.x] = bad;
+        if (threadIdx.x == 0) flags[t] = bad;
     } else {
         __syncthreads();
     }
-    uint16_t *d = dst + b * cols * dst_ld;
+    uint16_t *d = p.dst + b * p.cols * p.dst_ld;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int id = threadIdx.x + 256 * i;
         const int oc = id >> 3, rc = (id & 7) * 8;
         const int64_t col = c0 + oc, rr = r0 + rc;
-        if (col < cols && rr < dst_ld) {
+        if (col < p.cols && rr < p.dst_ld) {
             // rows rc .. rc + 7 share (r >> 3) = rc >> 3
             const int pc = (((oc >> 3) ^ ((rc >> 3) & 7)) << 3) + (oc & 7);
             uint32_t w[4];
@@ -260,9 +265,40 @@ __global__ __launch_bounds__(256) void transpose16_vec_kernel(const uint16_t *__
             for (int e = 0; e < 4; ++e)
                 w[e] = (uint32_t)tile[(rc + 2 * e) * 64 + pc] |
                        ((uint32_t)tile[(rc + 2 * e + 1) * 64 + pc] << 16);
-            *(u32x4 *)(d + col * dst_ld + rr) = u32x4{w[0], w[1], w[2], w[3]};
+            *(u32x4 *)(d + col * p.dst_ld + rr) = u32x4{w[0], w[1], w[2], w[3]};
         }
     }
+}
+
+// Same transpose with 16-byte accesses on both sides (cols, dst_ld and rows
+// multiples of 8, 16-byte aligned buffers): a 64x64 tile is read as 8-element
+// row chunks, and each output chunk gathers 8 consecutive rows of one column
+// from LDS.  The gather of a wave touches rows 8 apart, which share banks
+// for any row pitch that keeps chunks 16-byte aligned, so chunk c of row r
+// is stored at chunk c ^ ((r >> 3) & 7) instead of padding the rows.
+template <bool SCAN>
+__global__ __launch_bounds__(256) void transpose16_vec_kernel(const T16 p, uint32_t expmask,
+                                                              int32_t *flags) {
+    __shared__ __align__(16) uint16_t tile[64 * 64];
+    transpose16_vec_tile<SCAN>(p, blockIdx.x, tile, expmask, flags);
+}
+
+// Two independent transposes in one launch (workgroups [0, n0) do the first,
+// the rest the second), each with 16-byte accesses where its sizes and
+// alignment allow (vec0, vec1): the layout copies on the input side of a
+// channel-first call, one launch instead of two.
+__global__ __launch_bounds__(256) void transpose16_pair_kernel(const T16 p0, const T16 p1,
+                                                               int64_t n0, int vec0, int vec1) {
+    // 16-byte aligned: the 16-byte tile path stores whole chunks
+    __shared__ __align__(16) uint16_t tile[64][65];
+    const int64_t t = blockIdx.x;
+    const T16 &p = t < n0 ? p0 : p1;
+    const int64_t u = t < n0 ? t : t - n0;
+    if (t < n0 ? vec0 : vec1)
+        transpose16_vec_tile<false>(p, u, &tile[0][0], 0u, nullptr);
+    else
+        transpose16_tile<false>(p.src, p.dst, p.rows, p.cols, p.dst_ld, p.tiles_c, p.tiles_r, u,
+                                tile, 0u, nullptr);
 }
 
 // Block-diagonal super-group weights: dst[k][t][c'] (c' < sg, t < rs) is
@@ -303,6 +339,24 @@ int64_t transpose16_blocks(int64_t batch, int64_t cols, int64_t dst_ld) {
     return batch * ((cols + 63) / 64) * ((dst_ld + 63) / 64);
 }
 
+static T16 t16(const void *src, void *dst, int64_t rows, int64_t cols, int64_t dst_ld) {
+    T16 p;
+    p.src = (const uint16_t *)src;
+    p.dst = (uint16_t *)dst;
+    p.rows = rows;
+    p.cols = cols;
+    p.dst_ld = dst_ld;
+    p.tiles_c = (cols + 63) / 64;
+    p.tiles_r = (dst_ld + 63) / 64;
+    return p;
+}
+
+static bool t16_vec(const void *src, const void *dst, int64_t rows, int64_t cols,
+                    int64_t dst_ld) {
+    return cols % 8 == 0 && dst_ld % 8 == 0 && rows % 8 == 0 && (uintptr_t)src % 16 == 0 &&
+           (uintptr_t)dst % 16 == 0;
+}
+
 template <bool SCAN>
 static hipError_t transpose16_go(const void *src, void *dst, int64_t batch, int64_t rows,
                                  int64_t cols, int64_t dst_ld, uint32_t expmask, int32_t *flags,
@@ -311,12 +365,9 @@ static hipError_t transpose16_go(const void *src, void *dst, int64_t batch, int6
     const int64_t nb = batch * tiles_c * tiles_r;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
-    const bool vec = cols % 8 == 0 && dst_ld % 8 == 0 && rows % 8 == 0 &&
-                     (uintptr_t)src % 16 == 0 && (uintptr_t)dst % 16 == 0;
-    if (vec)
+    if (t16_vec(src, dst, rows, cols, dst_ld))
         hipLaunchKernelGGL(transpose16_vec_kernel<SCAN>, dim3((uint32_t)nb), dim3(256), 0, st,
-                           (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
-                           tiles_r, expmask, flags);
+                           t16(src, dst, rows, cols, dst_ld), expmask, flags);
     else
         hipLaunchKernelGGL(transpose16_kernel<SCAN>, dim3((uint32_t)nb), dim3(256), 0, st,
                            (const uint16_t *)src, (uint16_t *)dst, rows, cols, dst_ld, tiles_c,
@@ -327,6 +378,25 @@ static hipError_t transpose16_go(const void *src, void *dst, int64_t batch, int6
 hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t rows,
                               int64_t cols, int64_t dst_ld, hipStream_t st) {
     return transpose16_go<false>(src, dst, batch, rows, cols, dst_ld, 0u, nullptr, st);
+}
+
+hipError_t launch_transpose16_pair(const void *src0, void *dst0, int64_t batch0, int64_t rows0,
+                                   int64_t cols0, int64_t dst_ld0, const void *src1, void *dst1,
+                                   int64_t batch1, int64_t rows1, int64_t cols1, int64_t dst_ld1,
+                                   hipStream_t st) {
+    const int64_t n0 = batch0 * ((cols0 + 63) / 64) * ((dst_ld0 + 63) / 64);
+    const int64_t n1 = batch1 * ((cols1 + 63) / 64) * ((dst_ld1 + 63) / 64);
+    if (n0 <= 0 || n1 <= 0 || n0 + n1 > 0x7FFFFFFF) {
+        const hipError_t e = launch_transpose16(src0, dst0, batch0, rows0, cols0, dst_ld0, st);
+        if (e != hipSuccess) return e;
+        return launch_transpose16(src1, dst1, batch1, rows1, cols1, dst_ld1, st);
+    }
+    hipLaunchKernelGGL(transpose16_pair_kernel, dim3((uint32_t)(n0 + n1)), dim3(256), 0, st,
+                       t16(src0, dst0, rows0, cols0, dst_ld0),
+                       t16(src1, dst1, rows1, cols1, dst_ld1), n0,
+                       (int)t16_vec(src0, dst0, rows0, cols0, dst_ld0),
+                       (int)t16_vec(src1, dst1, rows1, cols1, dst_ld1));
+    return hipGetLastError();
 }
 
 hipError_t launch_transpose16_scan(const void *src, void *dst, int64_t batch, int64_t rows,

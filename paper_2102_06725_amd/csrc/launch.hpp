@@ -204,6 +204,12 @@ hipError_t launch_transpose16(const void *src, void *dst, int64_t batch, int64_t
 // transpose16_blocks(batch, cols, dst_ld) it launches, whether its tile of
 // src held an inf or NaN of the given operand dtype into flags[b].
 int64_t transpose16_blocks(int64_t batch, int64_t cols, int64_t dst_ld);
+// Two independent launch_transpose16 calls in one launch (two launches
+// when either cannot take the 16-byte kernel).
+hipError_t launch_transpose16_pair(const void *src0, void *dst0, int64_t batch0, int64_t rows0,
+                                   int64_t cols0, int64_t dst_ld0, const void *src1, void *dst1,
+                                   int64_t batch1, int64_t rows1, int64_t cols1, int64_t dst_ld1,
+                                   hipStream_t st);
 hipError_t launch_transpose16_scan(const void *src, void *dst, int64_t batch, int64_t rows,
                                    int64_t cols, int64_t dst_ld, int dtype, int32_t *flags,
                                    hipStream_t st);

@@ -65,6 +65,12 @@ def parse():
                     help="upper bound on the oracle CPU-baseline sample (0 disables it)")
     ap.add_argument("--flush-mib", type=int, default=1024,
                     help="scratch written before every cold timed step (0: warm only)")
+    ap.add_argument("--schedule", default="serial", choices=["serial", "train1", "train2"],
+                    help="order of the timed steps: serial = fwd, dgrad, wgrad layer by layer "
+                         "on one stream; train1 = the training order (forward over the layers, "
+                         "then backward in reverse) on one stream; train2 = the training order "
+                         "with each backward-weight pass on a second stream, started once the "
+                         "backward-data pass that yields its dy is queued")
     ap.add_argument("--no-events", action="store_true",
                     help="skip the event-instrumented steps (per-pass times, roofline)")
     ap.add_argument("--layers", default="",
@@ -679,8 +685,50 @@ def main():
             if ev is not None:
                 ev[i][3].record(stream)
 
+    side = torch.cuda.Stream(device=dev) if args.schedule == "train2" else None
+    ws_side = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev) if side else None
+    ready = [torch.cuda.Event() for _ in bufs]
+    joined = torch.cuda.Event()
+
+    def train_step():
+        """Forward over the layers in network order, then backward in reverse
+        order.  A layer's dy exists once the backward-data pass of the layer
+        after it has run, so its backward-weight pass may start there; with a
+        side stream it runs next to the rest of the backward-data chain."""
+        flag.zero_()
+        for b in bufs:
+            L = b.L
+            if b.x is not b.x_raw:
+                nc.check(nc.nnconv_pad_channels(b.x_raw.data_ptr(), b.x.data_ptr(),
+                                                L.n * L.h * L.w, L.c_alg, L.c, sptr), "pad")
+            nc.check(nc.nnconv_fwd(b.desc, b.x.data_ptr(), b.w.data_ptr(), b.y.data_ptr(), 1.0,
+                                   ws.data_ptr(), ws_bytes, sptr), "fwd")
+        for i in reversed(range(len(bufs))):
+            b = bufs[i]
+            if side is not None:
+                ready[i].record(stream)
+                side.wait_event(ready[i])
+                nc.check(nc.nnconv_wgrad(b.desc, b.x.data_ptr(), b.dy.data_ptr(),
+                                         b.dw.data_ptr(), nc.NNCONV_F32, inv_s, 0,
+                                         flag.data_ptr(), ws_side.data_ptr(), ws_bytes,
+                                         side.cuda_stream), "wgrad")
+            else:
+                nc.check(nc.nnconv_wgrad(b.desc, b.x.data_ptr(), b.dy.data_ptr(),
+                                         b.dw.data_ptr(), nc.NNCONV_F32, inv_s, 0,
+                                         flag.data_ptr(), ws.data_ptr(), ws_bytes, sptr),
+                         "wgrad")
+            if b.L.dgrad:
+                nc.check(nc.nnconv_dgrad(b.desc, b.dy.data_ptr(), b.w.data_ptr(),
+                                         b.dx.data_ptr(), 1.0, ws.data_ptr(), ws_bytes, sptr),
+                         "dgrad")
+        if side is not None:
+            joined.record(side)
+            stream.wait_event(joined)
+
+    timed_step = (lambda: one_step(None)) if args.schedule == "serial" else train_step
+
     for _ in range(args.warmup):
-        one_step(None)
+        timed_step()
     torch.cuda.synchronize()
 
     clock = ClockSampler()
@@ -691,7 +739,7 @@ def main():
     clock.armed = True
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        one_step(None)
+        timed_step()
     torch.cuda.synchronize()
     warm_s = time.perf_counter() - t0
     clock.armed = False
@@ -706,7 +754,7 @@ def main():
             torch.cuda.synchronize()
             clock.armed = True
             t0 = time.perf_counter()
-            one_step(None)
+            timed_step()
             torch.cuda.synchronize()
             cold_s += time.perf_counter() - t0
             clock.armed = False
@@ -865,6 +913,7 @@ def main():
                    "layer_passes": sum(3 if L.dgrad else 2 for L in layers),
                    "tflop_per_step": step_flops / 1e12,
                    "compulsory_gb_per_step": step_bytes / 1e9},
+        "schedule": args.schedule,
         "cache": {"headline": "cold" if cold_s is not None else "warm",
                   "flush_bytes": args.flush_mib * 1024 * 1024,
                   "cold": None if cold_s is None else {

@@ -159,7 +159,15 @@ typedef enum {
      * 64-channel slice of the input staged once per tile for all taps. */
     NNCONV_TILE_HALO_256x64 = 9,    /* 4 waves of 64x64 */
     NNCONV_TILE_HALO_256x128 = 10,  /* 4 waves of 128x64 */
-    NNCONV_TILE_HALO_256x64_2T = 11 /* 256x64, B tiles of two taps per barrier */
+    NNCONV_TILE_HALO_256x64_2T = 11, /* 256x64, B tiles of two taps per barrier */
+    /* Halo staging with the weight fragments loaded from L2 straight into
+     * registers several taps ahead and the next channel slice's halo loading
+     * during the current one (one workgroup per CU). */
+    NNCONV_TILE_HALO_R256x128 = 12, /* 4 waves of 128x64; taps within 64 raster
+                                       positions (3x3 on images up to 31 wide) */
+    NNCONV_TILE_HALO_R128x256 = 13, /* 4 waves of 128x64 side by side */
+    NNCONV_TILE_HALO_R224x256 = 14  /* 4 waves of 224x64 side by side; taps within
+                                       32 raster positions (3x3 up to 15 wide) */
 } nnconv_tile;
 
 /* nnconv_fwd / nnconv_dgrad with the tile forced (an nnconv_tile value).

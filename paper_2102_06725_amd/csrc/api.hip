@@ -206,11 +206,25 @@ int32_t plan_wgrad_direct_splits(const Geom &G) {
 }
 
 struct Regions {  // byte offsets into the caller's workspace
-    size_t a, b, c, d, e, total;
+    size_t a, b, c, d, e, f, total;
 };
 
+// Bytes of fragment-packed weights the register-weight halo tiles need for
+// this geometry and pass: 3x3 filters, stride 1, output the input's size,
+// one group, 64-channel multiples, taps within the larger halo buffer's
+// span.  0 when no such tile can run it.
+size_t hring_ws(const Geom &G, nnconv_pass pass) {
+    if (!(G.g == 1 && G.sh == 1 && G.sw == 1 && G.p == G.h && G.q == G.w &&
+          G.r * G.s == HRING_TAPS && G.cg % 64 == 0 && G.kg % 64 == 0 &&
+          (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw <= HALO_SPAN))
+        return 0;
+    if (pass == NNCONV_FWD) return hring_pack_bytes(G.kg, G.cg);
+    if (pass == NNCONV_DGRAD) return hring_pack_bytes(G.cg, G.kg);
+    return 0;
+}
+
 Regions fast_regions(const Geom &G, nnconv_pass pass) {
-    Regions R = {0, 0, 0, 0, 0, 0};
+    Regions R = {0, 0, 0, 0, 0, 0, 0};
     const size_t e2 = 2;
     const size_t xb = G.n * G.h * G.w * G.c * e2;
     const size_t yb = G.n * G.p * G.q * G.k * e2;
@@ -228,6 +242,7 @@ Regions fast_regions(const Geom &G, nnconv_pass pass) {
             R.b = take(wb);  // w [K][R][S][Cg]
             R.c = take(yb);  // y channel-last
         }
+        R.f = take(hring_ws(G, pass));  // packed weights (register-weight halo tiles)
     } else if (pass == NNCONV_DGRAD) {
         if (nchw) {
             R.a = take(yb);  // dy channel-last
@@ -237,6 +252,7 @@ Regions fast_regions(const Geom &G, nnconv_pass pass) {
         R.b = take(wb);      // w [g][R][S][Cg][Kg]
         // non-finite flags of the weight re-layout's workgroups
         R.e = take((size_t)transpose16_blocks(G.g, G.r * G.s * G.cg, G.kg) * 4);
+        R.f = take(hring_ws(G, pass));  // packed weights (register-weight halo tiles)
     } else {
         if (nchw) {
             R.a = take(xb);  // x channel-last
@@ -259,7 +275,7 @@ DWParams dw_params(const Geom &G, float alpha);
 // Depthwise workspace: the channel-last copies for NCHW calls, fp32 split
 // partials (backward-weight).
 Regions dw_regions(const Geom &G, nnconv_pass pass) {
-    Regions R = {0, 0, 0, 0, 0, 0};
+    Regions R = {0, 0, 0, 0, 0, 0, 0};
     const size_t xb = G.n * G.h * G.w * G.c * 2;
     const size_t yb = G.n * G.p * G.q * G.k * 2;
     size_t off = 0;
@@ -286,7 +302,7 @@ Regions dw_regions(const Geom &G, nnconv_pass pass) {
 // backward-data), then the super-grouped problem's own regions.
 Regions sg_regions(const Geom &G, nnconv_pass pass) {
     const Geom S = sg_geom(G);
-    Regions R = {0, 0, 0, 0, 0, 0};
+    Regions R = {0, 0, 0, 0, 0, 0, 0};
     const size_t wexp = pass == NNCONV_WGRAD ? 0 : align256(G.k * G.r * G.s * SUPER_GROUP * 2);
     const Regions in = fast_regions(S, pass);
     R.d = 0;            // expanded weights
@@ -294,6 +310,7 @@ Regions sg_regions(const Geom &G, nnconv_pass pass) {
     R.b = wexp + in.b;
     R.c = wexp + in.c;
     R.e = wexp + in.e;
+    R.f = wexp + in.f;
     R.total = wexp + in.total;
     return R;
 }
@@ -427,30 +444,54 @@ C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
 // halo-staged kernel (HaloConfig = id - HALO_TILE0); lower ones are
 // C64Config values.
 constexpr int HALO_TILE0 = 9;
-constexpr int HALO_CONFIGS = HALO_256x64_2T + 1;
+constexpr int HALO_CONFIGS = HALO_R224x256 + 1;
 bool halo_tile(int tile) { return tile >= HALO_TILE0 && tile < HALO_TILE0 + HALO_CONFIGS; }
+// the register-weight halo configurations (packed weights in the workspace)
+bool hring_cfg(int hc) { return hc == HALO_R256x128 || hc == HALO_R128x256 || hc == HALO_R224x256; }
 
 // Whether the halo-staged kernel can run this shape's forward and
 // backward-data passes (the geometry halo_supported() accepts, stated on the
 // convolution): one group, stride 1, output the input's size, 64-channel
 // multiples, taps spanning at most HALO_SPAN raster positions.
-bool halo_geom(const Geom &G) {
+bool halo_geom(const Geom &G, int tile) {
+    const HaloConfig hc = (HaloConfig)(tile - HALO_TILE0);
+    const bool regw = hring_cfg(hc);
     return G.g == 1 && G.sh == 1 && G.sw == 1 && G.p == G.h && G.q == G.w && G.cg % 64 == 0 &&
-           G.kg % 64 == 0 && G.r * G.s <= 32 &&
-           (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw <= HALO_SPAN;
+           G.kg % 64 == 0 && G.r * G.s <= 32 && (!regw || G.r * G.s == HRING_TAPS) &&
+           (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw <= halo_cfg_span(hc);
 }
 
 // The halo-staged kernel's tile for a stride-1 "same" implicit GEMM, or -1
 // for the 64-channel-slice kernel.  Measured on the ResNet-50 layers at
-// batch 256: on 3x3 filters over 7x7 images with wide outputs (where the
-// 64-channel-slice tiles stage each input pixel once per tap and per
-// 64-column tile) the halo tile is 2-3% faster than the pipelined 128x128
-// tile, forward and backward-data, and 8-14% faster than the single-stage
-// ones; it ties or loses on the wider images.  A 1x1 filter has no halo to
-// share: its tile is a plain GEMM tile, slower than the 64-channel-slice
-// ones (40-60% on the 7x7 1x1 layers).
-int pick_halo(const TNParams &p) {
-    if (p.ph[0].tap_count < 2 || !halo_supported(p) || p.a_w > 7 || p.ncols < 256) return -1;
+// batch 256 (forward and backward-data; times include the weight packing):
+//   - the register-weight tiles (packed weights in the workspace, 3x3
+//     filters): the 224x256 tile when the taps span at most 32 raster
+//     positions, the output columns are a multiple of 256 and its tiles
+//     fill between three quarters of the CUs and all of them in one round
+//     (the 14x14 256-channel layers: 224 tiles, 62 / 68 us against 66 / 71
+//     for the 16-wave 256x256 tile); the 256x128 tile on 7x7 images with at
+//     least 512 columns (66 / 71 us against 71 / 78 for the single-buffer
+//     halo tile, which those layers took before);
+//   - otherwise the single-buffer 256x64 halo tile on 3x3-like filters over
+//     7x7 images with at least 256 output columns, where the
+//     64-channel-slice tiles stage each input pixel once per tap and per
+//     64-column tile (2-3% faster than the pipelined 128x128 tile, 8-14%
+//     than the single-stage ones); it ties or loses on wider images.
+// A 1x1 filter has no halo to share: its tile is a plain GEMM tile, slower
+// than the 64-channel-slice ones (40-60% on the 7x7 1x1 layers).
+int device_cus();
+int pick_halo(const TNParams &p, bool pack) {
+    if (p.ph[0].tap_count < 2 || !halo_supported(p)) return -1;
+    if (pack && p.ph[0].tap_count == HRING_TAPS) {
+        const int64_t cus = device_cus();
+        const int64_t t224 = ((int64_t)p.ph[0].M + 223) / 224 * ((p.ncols + 255) / 256);
+        if (p.ncols % 256 == 0 && hring_supported(p, halo_cfg_span(HALO_R224x256)) &&
+            t224 <= cus && 4 * t224 >= 3 * cus)
+            return HALO_R224x256;
+        if (p.a_w <= 7 && p.ncols >= 512 && hring_supported(p, halo_cfg_span(HALO_R256x128)))
+            return HALO_R256x128;
+    }
+    if (p.a_w > 7 || p.ncols < 256) return -1;
     return HALO_256x64;
 }
 
@@ -488,8 +529,10 @@ bool c64_dgrad_shape(const Geom &G) { return G.kg % 64 == 0 && G.sh * G.sw <= MA
 
 // tile: a C64Config to force on the 64-channel-slice kernel, or -1 for the
 // per-shape pick.
+// pack: workspace for the register-weight halo tiles' packed weights
+// (hring_ws bytes), or null when the call has none.
 nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, float alpha,
-                       hipStream_t st, int tile = -1) {
+                       hipStream_t st, int tile = -1, void *pack = nullptr) {
     if (stem_shape(G)) {
         StemParams sp;
         sp.x = x;
@@ -552,10 +595,11 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
     if (G.cg % 64 == 0) {
         p.nphase = 1;
         p.ph[0] = phase_of(p.M, p.mi, p.mj, 0, 0, 0, t);
-        const int hc = halo_tile(tile) ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
+        const int hc = halo_tile(tile) ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p, pack != nullptr) : -1;
         if (hc >= 0) {
-            if (!halo_supported(p)) return NNCONV_ERR_UNSUPPORTED;
-            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, st));
+            if (!halo_cfg_supported(p, (HaloConfig)hc) || (hring_cfg(hc) && !pack))
+                return NNCONV_ERR_UNSUPPORTED;
+            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, pack, st));
         }
         const C64Config cfg =
             tile >= 0 ? (C64Config)tile : pick_c64_geom(G, p.M, G.kg, (int64_t)t * G.cg);
@@ -568,7 +612,7 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
 // output phase (h mod sigma_h, w mod sigma_w): within a phase every pixel
 // sees the same set of contributing taps.  wt is [g][R][S][Cg][Kg].
 nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx, float alpha,
-                         hipStream_t st, int tile = -1) {
+                         hipStream_t st, int tile = -1, void *pack = nullptr) {
     TNParams base = tn_base();
     base.a = dy;
     base.a_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
@@ -631,10 +675,11 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
             }
         }
         if (p.nphase == 0) return NNCONV_OK;
-        const int hc = halo_tile(tile) ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p) : -1;
+        const int hc = halo_tile(tile) ? tile - HALO_TILE0 : tile < 0 ? pick_halo(p, pack != nullptr) : -1;
         if (hc >= 0) {
-            if (!halo_supported(p)) return NNCONV_ERR_UNSUPPORTED;
-            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, st));
+            if (!halo_cfg_supported(p, (HaloConfig)hc) || (hring_cfg(hc) && !pack))
+                return NNCONV_ERR_UNSUPPORTED;
+            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, pack, st));
         }
         const C64Config cfg =
             tile >= 0 ? (C64Config)tile : pick_c64_geom(G, rows, G.cg, red_rows / rows);
@@ -923,8 +968,9 @@ static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void
     if (tile >= 0) {
         const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_fwd_shape(G) &&
                            aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
-                           (G.layout == NNCONV_NHWC || aligned(ws, 16));
-        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G)))
+                           (G.layout == NNCONV_NHWC || aligned(ws, 16)) &&
+                           (!halo_tile(tile) || !hring_cfg(tile - HALO_TILE0) || aligned(ws, 16));
+        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G, tile)))
             return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();
@@ -939,13 +985,14 @@ static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void
     const bool fast = fast_shape(G) && aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                       (G.layout == NNCONV_NHWC || aligned(ws, 16));
     if (!fast) return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
-    if (G.layout == NNCONV_NHWC) return fwd_fast(G, x, w, y, alpha, s, tile);
     const Regions R = fast_regions(G, NNCONV_FWD);
     char *base = (char *)ws;
+    void *pack = (hring_ws(G, NNCONV_FWD) > 0 && ws && aligned(ws, 16)) ? base + R.f : nullptr;
+    if (G.layout == NNCONV_NHWC) return fwd_fast(G, x, w, y, alpha, s, tile, pack);
     void *xt = base + R.a, *wt = base + R.b, *yt = base + R.c;
     TRY_HIP(launch_transpose16_pair(x, xt, G.n, G.c, G.h * G.w, G.c, w, wt, G.k, G.cg, G.r * G.s,
                                     G.cg, s));
-    if ((st = fwd_fast(G, xt, wt, yt, alpha, s, tile)) != NNCONV_OK) return st;
+    if ((st = fwd_fast(G, xt, wt, yt, alpha, s, tile, pack)) != NNCONV_OK) return st;
     return hip_status(launch_transpose16(yt, y, G.n, G.p * G.q, G.k, G.p * G.q, s));
 }
 
@@ -975,7 +1022,7 @@ static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const v
         const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_dgrad_shape(G) &&
                            aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
                            aligned(ws, 16);
-        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G)))
+        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G, tile)))
             return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();
@@ -1011,7 +1058,8 @@ static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const v
     int32_t *flags = (int32_t *)(base + R.e);
     TRY_HIP(launch_transpose16_scan(wkrsc, wt, G.g, G.kg, G.r * G.s * G.cg, G.kg, G.dtype, flags,
                                     s));
-    if ((st = dgrad_fast(G, dyn, wt, dxn, alpha, s, tile)) != NNCONV_OK) return st;
+    void *pack = hring_ws(G, NNCONV_DGRAD) > 0 ? base + R.f : nullptr;
+    if ((st = dgrad_fast(G, dyn, wt, dxn, alpha, s, tile, pack)) != NNCONV_OK) return st;
     // the implicit-GEMM kernels read dy zero-extended at every tap of a
     // stride phase: recompute the border pixels from the definition when a
     // weight is inf or NaN (with finite weights the kernel exits at once)

@@ -283,6 +283,18 @@ hipError_t launch_halo_t(HaloConfig cfg, TNParams &p, hipStream_t st) {
 
 }  // namespace
 
+int halo_tap_span(const TNParams &p) {
+    const TNPhase &F = p.ph[0];
+    int64_t lo = INT64_MAX, hi = INT64_MIN;
+    for (int t = 0; t < F.tap_count; ++t) {
+        const int64_t s = (int64_t)(p.ai_add + p.taps.dh[t]) * p.a_w + p.aj_add + p.taps.dw[t];
+        lo = s < lo ? s : lo;
+        hi = s > hi ? s : hi;
+    }
+    const int64_t span = hi - lo;
+    return span > 0x7FFFFFFF ? 0x7FFFFFFF : (int)span;
+}
+
 bool halo_supported(const TNParams &p) {
     if (p.nphase != 1 || p.groups != 1 || p.cr <= 0 || p.cr % 64 != 0 || p.a_c != p.cr)
         return false;
@@ -291,16 +303,22 @@ bool halo_supported(const TNParams &p) {
         F.oj_add != 0 || F.mi != p.a_h || F.mj != p.a_w || F.tap_start != 0 ||
         F.tap_count < 1 || F.tap_count > 32)
         return false;
-    int64_t lo = INT64_MAX, hi = INT64_MIN;
-    for (int t = 0; t < F.tap_count; ++t) {
-        const int64_t s = (int64_t)(p.ai_add + p.taps.dh[t]) * p.a_w + p.aj_add + p.taps.dw[t];
-        lo = s < lo ? s : lo;
-        hi = s > hi ? s : hi;
-    }
-    return hi - lo <= HALO_SPAN;
+    return halo_tap_span(p) <= HALO_SPAN;
 }
 
-hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, hipStream_t st) {
+int halo_cfg_span(HaloConfig cfg) {
+    return cfg == HALO_R256x128 ? 64 : cfg == HALO_R224x256 ? 32 : HALO_SPAN;
+}
+
+bool halo_cfg_supported(const TNParams &p, HaloConfig cfg) {
+    if (cfg == HALO_R256x128 || cfg == HALO_R128x256 || cfg == HALO_R224x256)
+        return hring_supported(p, halo_cfg_span(cfg));
+    return halo_supported(p);
+}
+
+hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, hipStream_t st) {
+    if (cfg == HALO_R256x128 || cfg == HALO_R128x256 || cfg == HALO_R224x256)
+        return launch_igemm_hring(dtype, cfg, p, pack, st);
     if (dtype == Half::id) return launch_halo_t<Half>(cfg, p, st);
     return launch_halo_t<BFloat>(cfg, p, st);
 }

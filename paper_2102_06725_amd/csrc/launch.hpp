@@ -104,10 +104,31 @@ hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hip
 constexpr int HALO_SPAN = 128;
 enum HaloConfig { HALO_256x64 = 0,      // 4 waves of 64x64
                   HALO_256x128 = 1,     // 4 waves of 128x64
-                  HALO_256x64_2T = 2 }; // 256x64 with the B tiles of two taps per step
+                  HALO_256x64_2T = 2,   // 256x64 with the B tiles of two taps per step
+                  // igemm_hring.hip: weight fragments from L2 into registers,
+                  // double-buffered halo (one workgroup per CU)
+                  HALO_R256x128 = 3,    // 4 waves of 128x64, taps within 64 raster positions
+                  HALO_R128x256 = 4,    // 4 waves of 128x64 side by side, taps within 128
+                  HALO_R224x256 = 5 };  // 4 waves of 224x64 side by side, taps within 32
 bool halo_supported(const TNParams &p);
-// hipErrorInvalidValue when !halo_supported(p)
-hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, hipStream_t st);
+// largest minus smallest raster shift of the taps of phase 0
+int halo_tap_span(const TNParams &p);
+// raster span of the taps the configuration's halo buffer holds
+int halo_cfg_span(HaloConfig cfg);
+// whether configuration cfg runs p (geometry, tap count and span)
+bool halo_cfg_supported(const TNParams &p, HaloConfig cfg);
+// hipErrorInvalidValue when !halo_cfg_supported(p, cfg); `pack` is used by
+// the register-weight configurations only (see launch_igemm_hring)
+hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, hipStream_t st);
+// The register-weight halo tiles (igemm_hring.hip) take 3x3 filters (9
+// taps) only.  They read the B operand packed in fragment order: `pack` is
+// caller-provided device memory of hring_pack_bytes(ncols, cr) bytes, which
+// launch_igemm_hring fills from p.b before the GEMM.
+constexpr int HRING_TAPS = 9;
+bool hring_supported(const TNParams &p, int span);
+size_t hring_pack_bytes(int64_t ncols, int64_t cr);
+hipError_t launch_igemm_hring(int dtype, HaloConfig cfg, TNParams &p, void *pack,
+                              hipStream_t st);
 
 // Forward pass for 8-channel (16-byte) channel-last pixels, 64 output
 // channels, groups 1, dilation 1 and a compiled filter size / stride (the

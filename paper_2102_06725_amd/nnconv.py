@@ -45,7 +45,18 @@ NNCONV_TILE_256x64_RING = 8
 NNCONV_TILE_HALO_256x64 = 9
 NNCONV_TILE_HALO_256x128 = 10
 NNCONV_TILE_HALO_256x64_2T = 11
-HALO_TILES = (NNCONV_TILE_HALO_256x64, NNCONV_TILE_HALO_256x128, NNCONV_TILE_HALO_256x64_2T)
+NNCONV_TILE_HALO_R256x128 = 12
+NNCONV_TILE_HALO_R128x256 = 13
+NNCONV_TILE_HALO_R224x256 = 14
+HALO_TILES = (NNCONV_TILE_HALO_256x64, NNCONV_TILE_HALO_256x128, NNCONV_TILE_HALO_256x64_2T,
+              NNCONV_TILE_HALO_R256x128, NNCONV_TILE_HALO_R128x256, NNCONV_TILE_HALO_R224x256)
+# largest raster span of the filter taps each halo tile's buffer holds
+HALO_TILE_SPAN = {NNCONV_TILE_HALO_256x64: 128, NNCONV_TILE_HALO_256x128: 128,
+                  NNCONV_TILE_HALO_256x64_2T: 128, NNCONV_TILE_HALO_R256x128: 64,
+                  NNCONV_TILE_HALO_R128x256: 128, NNCONV_TILE_HALO_R224x256: 32}
+# filter taps the halo tiles with register-held weights take (3x3 only)
+HALO_TILE_TAPS = {NNCONV_TILE_HALO_R256x128: 9, NNCONV_TILE_HALO_R128x256: 9,
+                  NNCONV_TILE_HALO_R224x256: 9}
 TILES = (NNCONV_TILE_256x256_8W, NNCONV_TILE_128x128_2S, NNCONV_TILE_128x128, NNCONV_TILE_128x64,
          NNCONV_TILE_256x256_16W, NNCONV_TILE_256x256_RING, NNCONV_TILE_256x128_RING,
          NNCONV_TILE_256x64_RING)

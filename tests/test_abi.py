@@ -99,7 +99,11 @@ def test_workspace_too_small(nnlib, layout):
 def test_workspace_sizes_are_deterministic_and_cover_partials(nnlib):
     d = good_desc(n=64, c=64, h=56, w=56, k=64, layout=nc.NNCONV_NHWC)
     st, f = nc.nnconv_workspace_size(d, nc.NNCONV_FWD)
-    assert st == 0 and f == 0                      # channel-last forward needs no scratch
+    # channel-last forward: only the weights packed in fragment order for the
+    # register-weight halo tiles (9 taps x 1 slice x 2 column blocks x 4 KB)
+    assert st == 0 and f == 9 * 1 * 2 * 4096
+    one = good_desc(n=64, c=64, h=56, w=56, k=64, r=1, s=1, pad=(0, 0), layout=nc.NNCONV_NHWC)
+    assert nc.nnconv_workspace_size(one, nc.NNCONV_FWD) == (0, 0)   # 1x1: no scratch
     st, w1 = nc.nnconv_workspace_size(d, nc.NNCONV_WGRAD)
     st, w2 = nc.nnconv_workspace_size(d, nc.NNCONV_WGRAD)
     assert w1 == w2 and w1 >= 64 * 9 * 64 * 4    # at least one fp32 partial of dw
@@ -184,7 +188,7 @@ def test_forced_tile_validation(nnlib):
     calls = (nc.nnconv_fwd_tile, nc.nnconv_dgrad_tile)
     for f in calls:
         assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, -1) == inv
-        for bad in (5, 12, 99):  # block-diagonal tile, out of range
+        for bad in (5, 15, 99):  # block-diagonal tile, out of range
             assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, bad) == uns
         # 16 reduction channels per tap: not the 64-channel-slice kernel
         small = nc.make_desc(2, 16, 8, 8, 16, 3, 3, pad=(1, 1))
@@ -216,6 +220,11 @@ def test_forced_tile_validation(nnlib):
         for d in not_same:
             for t in halo:
                 assert f(d, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, t) == uns
+        # the 320-row halo tile holds taps within 64 raster positions: a 3x3
+        # filter on a 32-pixel-wide image (span 66) is refused by it only
+        wide = nc.make_desc(2, 64, 8, 32, 64, 3, 3, pad=(1, 1))
+        assert f(wide, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None,
+                 nc.NNCONV_TILE_HALO_R256x128) == uns
 
 
 def test_noalloc_wgrad_validation(nnlib):

@@ -59,11 +59,25 @@ def test_forced_halo_tile_parity(nnlib, oracle_lib, tile, dtype, shape):
     case = U.Case(L, dtype=dtype, loss_scale=1.0, x_kind="normal", cfg=93,
                   layer_id=tile * 10 + HALO_SHAPES.index(shape))
     print("halo tile %d %s %s" % (tile, dtype, name), flush=True)
+    span = (r - 1) * dil * w + (s - 1) * dil   # raster positions between the outer taps
+    taps = nc.HALO_TILE_TAPS.get(tile)
+    if span > nc.HALO_TILE_SPAN[tile] or (taps is not None and r * s != taps):
+        # a halo buffer too small for the taps, or a tile compiled for
+        # another tap count: refused before anything runs
+        t = case.tensors()
+        with pytest.raises(nc.NNConvError) as e:
+            U.run_gpu(case, t, ("fwd",), tile=tile)
+        assert e.value.status == nc.NNCONV_ERR_UNSUPPORTED
+        with pytest.raises(nc.NNConvError) as e:
+            U.run_gpu(case, t, ("dgrad",), tile=tile)
+        assert e.value.status == nc.NNCONV_ERR_UNSUPPORTED
+        return
     U.full_parity(case, passes=("fwd", "dgrad"), tile=tile)
 
 
 @pytest.mark.parametrize("tile", [nc.NNCONV_TILE_256x256_RING, nc.NNCONV_TILE_256x128_RING,
-                                  nc.NNCONV_TILE_HALO_256x64, nc.NNCONV_TILE_HALO_256x128])
+                                  nc.NNCONV_TILE_HALO_256x64, nc.NNCONV_TILE_HALO_256x128,
+                                  nc.NNCONV_TILE_HALO_R256x128, nc.NNCONV_TILE_HALO_R128x256])
 def test_forced_tile_nchw_and_alpha(nnlib, oracle_lib, tile):
     """NCHW calls go through the channel-last kernels via the workspace; a
     non-unit alpha scales before the single rounding."""

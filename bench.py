@@ -65,12 +65,13 @@ def parse():
                     help="upper bound on the oracle CPU-baseline sample (0 disables it)")
     ap.add_argument("--flush-mib", type=int, default=1024,
                     help="scratch written before every cold timed step (0: warm only)")
-    ap.add_argument("--schedule", default="serial", choices=["serial", "train1", "train2"],
+    ap.add_argument("--schedule", default="train2", choices=["serial", "train1", "train2"],
                     help="order of the timed steps: serial = fwd, dgrad, wgrad layer by layer "
                          "on one stream; train1 = the training order (forward over the layers, "
-                         "then backward in reverse) on one stream; train2 = the training order "
-                         "with each backward-weight pass on a second stream, started once the "
-                         "backward-data pass that yields its dy is queued")
+                         "then backward in reverse) on one stream; train2 (the headline) = the "
+                         "training order with each backward-weight pass on a second stream, "
+                         "started once the backward-data pass that yields its dy is queued; "
+                         "any other schedule's cold time is reported beside it as 'serial'")
     ap.add_argument("--no-events", action="store_true",
                     help="skip the event-instrumented steps (per-pass times, roofline)")
     ap.add_argument("--layers", default="",
@@ -758,6 +759,18 @@ def main():
             torch.cuda.synchronize()
             cold_s += time.perf_counter() - t0
             clock.armed = False
+    # The serial schedule's cold time beside the headline (one stream, layer
+    # by layer: the sum of the passes' kernel times with no overlap).
+    serial_s = None
+    if flush is not None and args.schedule != "serial":
+        serial_s = 0.0
+        for k in range(args.steps):
+            flush.fill_(k & 0xFF)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            one_step(None)
+            torch.cuda.synchronize()
+            serial_s += time.perf_counter() - t0
     clock.close()
     elapsed = cold_s if cold_s is not None else warm_s
     if int(flag.item()) != 0:
@@ -913,7 +926,13 @@ def main():
                    "layer_passes": sum(3 if L.dgrad else 2 for L in layers),
                    "tflop_per_step": step_flops / 1e12,
                    "compulsory_gb_per_step": step_bytes / 1e9},
-        "schedule": args.schedule,
+        "schedule": {"headline": args.schedule,
+                     "note": "train2: forward over the layers in network order, then backward in "
+                             "reverse order with each backward-weight pass on a second stream "
+                             "(default priority), queued once the backward-data pass that yields "
+                             "its dy is queued, as a training step can run them",
+                     "serial_cold": None if serial_s is None else {
+                         "ms_per_step": serial_s / args.steps * 1e3, "value": rate(serial_s)}},
         "cache": {"headline": "cold" if cold_s is not None else "warm",
                   "flush_bytes": args.flush_mib * 1024 * 1024,
                   "cold": None if cold_s is None else {

@@ -47,6 +47,8 @@ HALO_SHAPES = [
     ("h5", 2, 64, 8, 12, 128, 5, 5, 2, 1),       # 25 taps
     ("hdil", 2, 128, 11, 9, 64, 3, 3, 2, 2),     # dilation 2
     ("hlong", 2, 512, 5, 6, 256, 3, 3, 1, 1),    # 8 channel slices
+    ("h64", 3, 64, 20, 24, 64, 3, 3, 1, 1),      # 64 -> 64: 1440 rows, a ragged 448-row tile
+    ("h64w56", 1, 64, 9, 56, 64, 3, 3, 1, 1),    # 64 -> 64 on a 56-wide image (span 114)
 ]
 
 

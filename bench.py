@@ -197,7 +197,7 @@ def write_per_layer(path, layers, ev_steps, steps):
 # Sources that determine the forward launches (dispatch plans and kernels);
 # stored HBM-traffic counters are reported only while these are unchanged.
 FWD_SOURCES = ("api.hip", "common.hpp", "igemm_c8.hip", "igemm_c64.hip", "igemm_halo.hip",
-               "igemm_store.hpp", "launch.hpp", "stem.hip")
+               "igemm_hring.hip", "igemm_store.hpp", "launch.hpp", "stem.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "igemm_fwd_traffic_resnet50_b256.txt")
 COPY_ROW_BYTES = 128    # calibration copy: rows of 64 fp16 channels
 
@@ -231,23 +231,38 @@ def stored_traffic(kind="mfma"):
         return None
 
 
-FWD_KERNEL = re.compile(r"nnconv::(igemm|stem_fwd|dw_fwd|dwt_fwd)")
+FWD_KERNEL = re.compile(r"nnconv::(igemm|stem_fwd|dw_fwd|dwt_fwd|pack_hring)")
 
 
-def is_forward_launch(names, i):
-    """In this script's launch order (flag clear, then per layer: optional
-    stem channel padding, forward, backward-data kernels, backward-weight
-    kernel and its reduction) a forward launch is an implicit-GEMM, stem or
-    depthwise-forward dispatch that follows a non-library dispatch, a split
-    reduction or a padding copy."""
-    n = names[i]
-    if "nnconv::" not in n or not ("igemm" in n or "stem_fwd" in n or "dw_fwd" in n or
-                                   "dwt_fwd" in n):
-        return False
-    if i == 0:
-        return True
-    prev = names[i - 1]
+def _main_fwd_kernel(n):
+    return "nnconv::" in n and ("igemm" in n or "stem_fwd" in n or "dw_fwd" in n or
+                                "dwt_fwd" in n)
+
+
+def _opens_call(prev):
+    """A dispatch after which the next library call starts: a non-library
+    dispatch, a split reduction (end of a backward-weight call) or a padding
+    copy (the stem's channel padding)."""
     return "nnconv::" not in prev or "wgrad_reduce" in prev or "pad_channels" in prev
+
+
+def forward_calls(names):
+    """Dispatch indices of each forward call in a trace of the serial schedule
+    (flag clear, then per layer: optional stem channel padding, forward,
+    backward-data kernels, backward-weight kernel and its reduction).  A
+    forward call is an implicit-GEMM, stem or depthwise-forward dispatch that
+    opens a call, with the weight-packing dispatch of the register-weight halo
+    tiles in front of it when there is one."""
+    calls = []
+    for i, n in enumerate(names):
+        if not _main_fwd_kernel(n):
+            continue
+        j, pre = i - 1, []
+        if j >= 0 and "pack_hring" in names[j]:
+            pre, j = [j], j - 1
+        if j < 0 or _opens_call(names[j]):
+            calls.append(pre + [i])
+    return calls
 
 
 def summarize_profile(args):
@@ -269,9 +284,10 @@ def summarize_profile(args):
     out = []
 
     def fwd_launches(names):
-        """Forward launches after the warm-up steps, with their layer index."""
-        f = [i for i in range(len(names)) if is_forward_launch(names, i)][skip:]
-        return [(i, j % nl) for j, i in enumerate(f)]
+        """Forward calls (dispatch index lists) after the warm-up steps, with
+        their layer index."""
+        f = forward_calls(names)[skip:]
+        return [(c, j % nl) for j, c in enumerate(f)]
 
     def family(n):
         return n.split("(")[0].replace("void ", "") if "nnconv::" in n else "(torch / runtime)"
@@ -292,14 +308,14 @@ def summarize_profile(args):
             out.append("%-72s %7d %12.1f %10.2f %6.2f" % (k[:72], v[0], v[1] / 1e3,
                                                           v[1] / v[0] / 1e3, 100.0 * v[1] / tot))
         fwd = fwd_launches(names)
-        out.append("forward launches (after %d warm-up ones): %d, average %.2f us, total %.1f us"
-                   % (skip, len(fwd), sum(dur[i] for i, _ in fwd) / max(1, len(fwd)) / 1e3,
-                      sum(dur[i] for i, _ in fwd) / 1e3))
+        cdur = [sum(dur[i] for i in c) for c, _ in fwd]
+        out.append("forward calls (after %d warm-up ones): %d, average %.2f us, total %.1f us"
+                   % (skip, len(fwd), sum(cdur) / max(1, len(fwd)) / 1e3, sum(cdur) / 1e3))
         for kind, members in sets:
-            sel = [i for i, li in fwd if li in members]
+            sel = [d for d, (_, li) in zip(cdur, fwd) if li in members]
             if sel:
-                out.append("forward launches of the %s-bound layers: %d, average %.2f us"
-                           % (kind, len(sel), sum(dur[i] for i in sel) / len(sel) / 1e3))
+                out.append("forward calls of the %s-bound layers: %d, average %.2f us"
+                           % (kind, len(sel), sum(sel) / len(sel) / 1e3))
         # the roofline launches of a run without --no-events: the runs of
         # forward kernels right after each loss-scaler initialisation (the
         # MFMA-bound set first, then the HBM-bound one)
@@ -312,8 +328,9 @@ def summarize_profile(args):
                 if j > i + 1:
                     runs.append(range(i + 1, j))
         for kind, run in zip([k for k, m in sets if m], runs):
-            out.append("roofline launches (%s-bound set, back to back): %d, average %.2f us"
-                       % (kind, len(run), sum(dur[i] for i in run) / len(run) / 1e3))
+            ncalls = sum(1 for i in run if "pack_hring" not in names[i])
+            out.append("roofline calls (%s-bound set, back to back): %d, average %.2f us"
+                       % (kind, ncalls, sum(dur[i] for i in run) / ncalls / 1e3))
     for path in sorted(glob.glob(os.path.join(args.summarize_profile, "**",
                                               "*counter_collection.csv"), recursive=True)):
         allrows = list(csv.DictReader(open(path)))
@@ -335,10 +352,10 @@ def summarize_profile(args):
             fwd = fwd_launches(names)
             out.append(line)
             for kind, members in sets:
-                sel = [i for i, li in fwd if li in members]
+                sel = [c for c, li in fwd if li in members]
                 if not sel:
                     continue
-                per = sum(vals[i] for i in sel) / len(sel) * 1024.0
+                per = sum(vals[i] for c in sel for i in c) / len(sel) * 1024.0
                 out.append("  forward launches of the %s-bound layers: %d, %.1f MB per launch as "
                            "counted%s" % (kind, len(sel), per / 1e6, "" if factor is None else
                                           ", %.1f MB scaled" % (per * factor / 1e6)))
@@ -365,11 +382,13 @@ def summarize_profile(args):
         # backward-weight for the split-K kernels and their reduction,
         # backward-data for the rest
         layer_of, li = {}, None
-        fwd_pos = {i: j for j, (i, _) in enumerate(fwd_launches(names))}
+        calls = forward_calls(names)
+        call_of = {i: j for j, c in enumerate(calls) for i in c}
         for pos, k in enumerate(ids):
-            fwd = is_forward_launch(names, pos)
-            if fwd:
-                li = layers[fwd_pos[pos] % nl].name if pos in fwd_pos else None
+            fwd = pos in call_of
+            if fwd and pos == calls[call_of[pos]][0]:
+                j = call_of[pos] - skip
+                li = layers[j % nl].name if j >= 0 else None
             nm = names[pos]
             ps = "fwd" if fwd else ("wgrad" if "wgrad" in nm else "dgrad")
             layer_of[k] = None if li is None else (li, ps)

@@ -40,9 +40,17 @@ def test_forward_launch_classifier():
         "nnconv::dwt_fwd_kernel<nnconv::Half, 3, 1, 4, false, true>",                # dgrad
         "nnconv::dwt_wgrad_kernel<nnconv::Half, 3, 1, 4>",
         "nnconv::wgrad_reduce_vec_kernel<2, 16>",
+        # a register-weight halo layer: packing + GEMM in both passes
+        "nnconv::pack_hring_b_kernel",                                               # fwd
+        "nnconv::igemm_hring_kernel<nnconv::Half, 224, 256, 1, 4, 256, 9, 3>",       # fwd
+        "nnconv::transpose16_vec_kernel<true>",
+        "nnconv::pack_hring_b_kernel",
+        "nnconv::igemm_hring_kernel<nnconv::Half, 224, 256, 1, 4, 256, 9, 3>",       # dgrad
+        "nnconv::dgrad_border_kernel<nnconv::Half>",
+        "nnconv::wgrad_splitk_kernel<nnconv::Half, 256, 256, 4, 4, 32, 2, false>",
+        "nnconv::wgrad_reduce_vec_kernel<2, 16>",
     ]
-    got = [i for i in range(len(names)) if B.is_forward_launch(names, i)]
-    assert got == [2, 5, 10]
+    assert B.forward_calls(names) == [[2], [5], [10], [14, 15]]
 
 
 def test_compulsory_bytes_by_hand():

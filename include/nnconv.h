@@ -162,12 +162,15 @@ typedef enum {
     NNCONV_TILE_HALO_256x64_2T = 11, /* 256x64, B tiles of two taps per barrier */
     /* Halo staging with the weight fragments loaded from L2 straight into
      * registers several taps ahead and the next channel slice's halo loading
-     * during the current one (one workgroup per CU). */
+     * during the current one (one workgroup per CU unless stated). */
     NNCONV_TILE_HALO_R256x128 = 12, /* 4 waves of 128x64; taps within 64 raster
                                        positions (3x3 on images up to 31 wide) */
     NNCONV_TILE_HALO_R128x256 = 13, /* 4 waves of 128x64 side by side */
-    NNCONV_TILE_HALO_R224x256 = 14  /* 4 waves of 224x64 side by side; taps within
+    NNCONV_TILE_HALO_R224x256 = 14, /* 4 waves of 224x64 side by side; taps within
                                        32 raster positions (3x3 up to 15 wide) */
+    NNCONV_TILE_HALO_R256x64S = 15  /* 4 waves of 64x64, a single 64-channel
+                                       reduction slice (Cg = 64 forward, Kg = 64
+                                       backward-data), two workgroups per CU */
 } nnconv_tile;
 
 /* nnconv_fwd / nnconv_dgrad with the tile forced (an nnconv_tile value).

@@ -444,20 +444,23 @@ C64Config pick_c64(int64_t m, int64_t ncols, int64_t red) {
 // halo-staged kernel (HaloConfig = id - HALO_TILE0); lower ones are
 // C64Config values.
 constexpr int HALO_TILE0 = 9;
-constexpr int HALO_CONFIGS = HALO_R224x256 + 1;
+constexpr int HALO_CONFIGS = HALO_R256x64S + 1;
 bool halo_tile(int tile) { return tile >= HALO_TILE0 && tile < HALO_TILE0 + HALO_CONFIGS; }
 // the register-weight halo configurations (packed weights in the workspace)
-bool hring_cfg(int hc) { return hc == HALO_R256x128 || hc == HALO_R128x256 || hc == HALO_R224x256; }
+bool hring_cfg(int hc) { return hring_config(hc); }
 
 // Whether the halo-staged kernel can run this shape's forward and
 // backward-data passes (the geometry halo_supported() accepts, stated on the
 // convolution): one group, stride 1, output the input's size, 64-channel
-// multiples, taps spanning at most HALO_SPAN raster positions.
-bool halo_geom(const Geom &G, int tile) {
+// multiples, taps spanning at most HALO_SPAN raster positions.  `red` is the
+// pass's reduction channel count (Cg forward, Kg backward-data), which the
+// single-slice tile needs to be 64.
+bool halo_geom(const Geom &G, int tile, int64_t red) {
     const HaloConfig hc = (HaloConfig)(tile - HALO_TILE0);
     const bool regw = hring_cfg(hc);
     return G.g == 1 && G.sh == 1 && G.sw == 1 && G.p == G.h && G.q == G.w && G.cg % 64 == 0 &&
            G.kg % 64 == 0 && G.r * G.s <= 32 && (!regw || G.r * G.s == HRING_TAPS) &&
+           (hc != HALO_R256x64S || red == 64) &&
            (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw <= halo_cfg_span(hc);
 }
 
@@ -465,7 +468,10 @@ bool halo_geom(const Geom &G, int tile) {
 // for the 64-channel-slice kernel.  Measured on the ResNet-50 layers at
 // batch 256 (forward and backward-data; times include the weight packing):
 //   - the register-weight tiles (packed weights in the workspace, 3x3
-//     filters): the 224x256 tile when the taps span at most 32 raster
+//     filters): the single-slice 256x64 tile for a 64-channel reduction
+//     into at most 64 columns (the 56x56 64-channel 3x3 layers: 82 / 86 us
+//     against 101 / 102 for the 128x64 64-channel-slice tile, the packing
+//     included); the 224x256 tile when the taps span at most 32 raster
 //     positions, the output columns are a multiple of 256 and its tiles
 //     fill between three quarters of the CUs and all of them in one round
 //     (the 14x14 256-channel layers: 224 tiles, 62 / 68 us against 66 / 71
@@ -483,6 +489,8 @@ int device_cus();
 int pick_halo(const TNParams &p, bool pack) {
     if (p.ph[0].tap_count < 2 || !halo_supported(p)) return -1;
     if (pack && p.ph[0].tap_count == HRING_TAPS) {
+        if (p.cr == 64 && p.ncols <= 64 && halo_cfg_supported(p, HALO_R256x64S))
+            return HALO_R256x64S;
         const int64_t cus = device_cus();
         const int64_t t224 = ((int64_t)p.ph[0].M + 223) / 224 * ((p.ncols + 255) / 256);
         if (p.ncols % 256 == 0 && hring_supported(p, halo_cfg_span(HALO_R224x256)) &&
@@ -970,7 +978,7 @@ static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void
                            aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                            (G.layout == NNCONV_NHWC || aligned(ws, 16)) &&
                            (!halo_tile(tile) || !hring_cfg(tile - HALO_TILE0) || aligned(ws, 16));
-        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G, tile)))
+        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G, tile, G.cg)))
             return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();
@@ -1022,7 +1030,7 @@ static nnconv_status dgrad_impl(const nnconv_desc *desc, const void *dy, const v
         const bool dense = !dw_shape(G) && !sg_shape(G) && fast_shape(G) && c64_dgrad_shape(G) &&
                            aligned(dy, 16) && aligned(w, 16) && aligned(dx, 16) &&
                            aligned(ws, 16);
-        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G, tile)))
+        if (!tile_ok(tile) || !dense || (halo_tile(tile) && !halo_geom(G, tile, G.kg)))
             return NNCONV_ERR_UNSUPPORTED;
     }
     clear_stale_error();

@@ -311,14 +311,13 @@ int halo_cfg_span(HaloConfig cfg) {
 }
 
 bool halo_cfg_supported(const TNParams &p, HaloConfig cfg) {
-    if (cfg == HALO_R256x128 || cfg == HALO_R128x256 || cfg == HALO_R224x256)
-        return hring_supported(p, halo_cfg_span(cfg));
+    if (hring_config(cfg))
+        return hring_supported(p, halo_cfg_span(cfg)) && (cfg != HALO_R256x64S || p.cr == 64);
     return halo_supported(p);
 }
 
 hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, hipStream_t st) {
-    if (cfg == HALO_R256x128 || cfg == HALO_R128x256 || cfg == HALO_R224x256)
-        return launch_igemm_hring(dtype, cfg, p, pack, st);
+    if (hring_config(cfg)) return launch_igemm_hring(dtype, cfg, p, pack, st);
     if (dtype == Half::id) return launch_halo_t<Half>(cfg, p, st);
     return launch_halo_t<BFloat>(cfg, p, st);
 }

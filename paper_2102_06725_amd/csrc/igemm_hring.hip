@@ -40,13 +40,16 @@ constexpr int KS = 4;   // 16-deep k-steps per 64-channel slice
 
 }  // namespace hring
 
-// BM x BN output tile, WM x WN waves (one per SIMD), HR halo rows per LDS
-// buffer, NT filter taps, D steps of weight fragments in flight (D divides
-// NT: a channel slice is unrolled over its taps, so every ring index and
-// every load is fixed at compile time and the compiler's wait counts are
-// exact).
-template <class T, int BM, int BN, int WM, int WN, int HR, int NT, int D>
-__global__ __launch_bounds__(WM * WN * 64, 1)
+// BM x BN output tile, WM x WN waves, HR halo rows per LDS buffer, NT filter
+// taps, D steps of weight fragments in flight (D divides NT: a channel slice
+// is unrolled over its taps, so every ring index and every load is fixed at
+// compile time and the compiler's wait counts are exact).  NB halo buffers:
+// 2 (double-buffered slices, one workgroup per CU), or 1 for a reduction of
+// a single 64-channel slice (the host checks cr == 64), where a tile stages
+// its halo once and OCC workgroups share a CU, one's staging and output
+// stage covered by the others' matrix-core work.
+template <class T, int BM, int BN, int WM, int WN, int HR, int NT, int D, int NB, int OCC>
+__global__ __launch_bounds__(WM * WN * 64, OCC)
 void igemm_hring_kernel(const TNParams P) {
     using namespace hring;
     constexpr int NW = WM * WN;
@@ -54,7 +57,8 @@ void igemm_hring_kernel(const TNParams P) {
     constexpr int FM = WTM / 32, FN = WTN / 32;
     constexpr int H_LD = HR / (RPI * NW);  // halo loads per lane per slice
     constexpr int H_SLOTS = HR * BKC;
-    constexpr int ZERO = 2 * H_SLOTS;      // one row of zeros
+    constexpr int ZERO = NB * H_SLOTS;     // one row of zeros
+    static_assert(NB == 1 || NB == 2, "halo buffers");
     // the output stage reuses the LDS for the BM x BN tile, which can be
     // larger than the two halo buffers
     constexpr int LDS_SLOTS = ZERO + BKC > BM * BN / 8 ? ZERO + BKC : BM * BN / 8;
@@ -234,16 +238,16 @@ void igemm_hring_kernel(const TNParams P) {
     step_addrs(0, 0, aa);
     read_a(aa, 0, fa[0]);
     for (int c = 0; c < nslices; ++c) {
-        const int hb = c & 1;
+        const int hb = NB == 2 ? (c & 1) : 0;
         // the next slice's halo: into registers at the first step, into the
         // other LDS buffer (free since the barrier that opened this slice)
         // at the last, then the barrier that opens the next slice
-        load_halo(c + 1);
+        if constexpr (NB == 2) load_halo(c + 1);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const int k = c * NT + t;
             uint32_t aa1[FM];
-            step_addrs(t + 1 < NT ? t + 1 : 0, t + 1 < NT ? hb : hb ^ 1, aa1);
+            step_addrs(t + 1 < NT ? t + 1 : 0, t + 1 < NT ? hb : (hb ^ (NB - 1)), aa1);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 const int cur = ks & 1, nxt = cur ^ 1;
@@ -263,11 +267,13 @@ void igemm_hring_kernel(const TNParams P) {
 #pragma unroll
             for (int i = 0; i < FM; ++i) aa[i] = aa1[i];
         }
-        store_halo(hb ^ 1);
-        // every wave has stored its share of the next slice's halo and is
-        // done with this slice's
-        barrier_lds();
-        read_a(aa, 0, fa[0]);
+        if constexpr (NB == 2) {
+            store_halo(hb ^ 1);
+            // every wave has stored its share of the next slice's halo and
+            // is done with this slice's
+            barrier_lds();
+            read_a(aa, 0, fa[0]);
+        }
     }
 
     store_tile<T, BM, BN, WM, WN, FM, FN>(acc, &lds[0], P, F, m0, n0, 0);
@@ -318,9 +324,9 @@ hipError_t launch_hring_pack(const TNParams &p, void *dst, hipStream_t st) {
 
 namespace {
 
-template <class T, int BM, int BN, int WM, int WN, int HR>
+template <class T, int BM, int BN, int WM, int WN, int HR, int NB = 2, int OCC = 1>
 hipError_t launch_hring_cfg(TNParams &p, hipStream_t st) {
-    if (!hring_supported(p, HR - BM)) return hipErrorInvalidValue;
+    if (!hring_supported(p, HR - BM) || (NB == 1 && p.cr != 64)) return hipErrorInvalidValue;
     p.tiles_n = (p.ncols + BN - 1) / BN;
     const int64_t tiles_m = (p.ph[0].M + BM - 1) / BM;
     p.ph[0].tiles_m = (int32_t)tiles_m;
@@ -329,12 +335,12 @@ hipError_t launch_hring_cfg(TNParams &p, hipStream_t st) {
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     // 3x3 filters (the host admits no other tap count)
-    hipLaunchKernelGGL((igemm_hring_kernel<T, BM, BN, WM, WN, HR, HRING_TAPS, 3>), dim3((uint32_t)nb),
+    hipLaunchKernelGGL((igemm_hring_kernel<T, BM, BN, WM, WN, HR, HRING_TAPS, 3, NB, OCC>), dim3((uint32_t)nb),
                        dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
 
-// Configurations (one workgroup of 4 waves per CU):
+// Configurations (4 waves; one workgroup per CU but the single-slice one):
 //   256x128: 4 waves of 128x64, halo of 320 rows (taps within 64 raster
 //            positions: 3x3 on images up to 31 wide), 80 KB of LDS
 //   128x256: 4 waves of 128x64 side by side, halo of 256 rows (within 128:
@@ -342,11 +348,15 @@ hipError_t launch_hring_cfg(TNParams &p, hipStream_t st) {
 //   224x256: 4 waves of 224x64 side by side, halo of 256 rows (within 32:
 //            up to 15 wide), 64 KB; 224 tiles for the 14x14 3x3 layers at
 //            batch 256: one round on 256 CUs
+//   256x64 single slice: 4 waves of 64x64, one halo buffer of 384 rows
+//            (within 128), 48 KB, two workgroups per CU: 64-channel
+//            reductions with at most 64 output columns per tile
 template <class T>
 hipError_t launch_hring_t(HaloConfig cfg, TNParams &p, hipStream_t st) {
     switch (cfg) {
         case HALO_R256x128: return launch_hring_cfg<T, 256, 128, 2, 2, 320>(p, st);
         case HALO_R224x256: return launch_hring_cfg<T, 224, 256, 1, 4, 256>(p, st);
+        case HALO_R256x64S: return launch_hring_cfg<T, 256, 64, 4, 1, 384, 1, 2>(p, st);
         case HALO_R128x256:
         default: return launch_hring_cfg<T, 128, 256, 1, 4, 256>(p, st);
     }
@@ -360,7 +370,7 @@ bool hring_supported(const TNParams &p, int span) {
 
 hipError_t launch_igemm_hring(int dtype, HaloConfig cfg, TNParams &p, void *pack,
                               hipStream_t st) {
-    if (!hring_supported(p, halo_cfg_span(cfg))) return hipErrorInvalidValue;
+    if (!halo_cfg_supported(p, cfg)) return hipErrorInvalidValue;
     hipError_t e = launch_hring_pack(p, pack, st);
     if (e != hipSuccess) return e;
     TNParams q = p;

@@ -109,7 +109,11 @@ enum HaloConfig { HALO_256x64 = 0,      // 4 waves of 64x64
                   // double-buffered halo (one workgroup per CU)
                   HALO_R256x128 = 3,    // 4 waves of 128x64, taps within 64 raster positions
                   HALO_R128x256 = 4,    // 4 waves of 128x64 side by side, taps within 128
-                  HALO_R224x256 = 5 };  // 4 waves of 224x64 side by side, taps within 32
+                  HALO_R224x256 = 5,    // 4 waves of 224x64 side by side, taps within 32
+                  HALO_R256x64S = 6 };  // 4 waves of 64x64, single 64-channel slice
+                                        // (cr == 64), two workgroups per CU
+// the register-weight configurations are the ones from HALO_R256x128 on
+inline bool hring_config(int cfg) { return cfg >= HALO_R256x128 && cfg <= HALO_R256x64S; }
 bool halo_supported(const TNParams &p);
 // largest minus smallest raster shift of the taps of phase 0
 int halo_tap_span(const TNParams &p);
@@ -121,7 +125,7 @@ bool halo_cfg_supported(const TNParams &p, HaloConfig cfg);
 // the register-weight configurations only (see launch_igemm_hring)
 hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, hipStream_t st);
 // The register-weight halo tiles (igemm_hring.hip) take 3x3 filters (9
-// taps) only.  They read the B operand packed in fragment order: `pack` is
+// taps) only, HALO_R256x64S a single 64-channel slice (cr == 64) too.  They read the B operand packed in fragment order: `pack` is
 // caller-provided device memory of hring_pack_bytes(ncols, cr) bytes, which
 // launch_igemm_hring fills from p.b before the GEMM.
 constexpr int HRING_TAPS = 9;

@@ -48,15 +48,20 @@ NNCONV_TILE_HALO_256x64_2T = 11
 NNCONV_TILE_HALO_R256x128 = 12
 NNCONV_TILE_HALO_R128x256 = 13
 NNCONV_TILE_HALO_R224x256 = 14
+NNCONV_TILE_HALO_R256x64S = 15
 HALO_TILES = (NNCONV_TILE_HALO_256x64, NNCONV_TILE_HALO_256x128, NNCONV_TILE_HALO_256x64_2T,
-              NNCONV_TILE_HALO_R256x128, NNCONV_TILE_HALO_R128x256, NNCONV_TILE_HALO_R224x256)
+              NNCONV_TILE_HALO_R256x128, NNCONV_TILE_HALO_R128x256, NNCONV_TILE_HALO_R224x256,
+              NNCONV_TILE_HALO_R256x64S)
 # largest raster span of the filter taps each halo tile's buffer holds
 HALO_TILE_SPAN = {NNCONV_TILE_HALO_256x64: 128, NNCONV_TILE_HALO_256x128: 128,
                   NNCONV_TILE_HALO_256x64_2T: 128, NNCONV_TILE_HALO_R256x128: 64,
-                  NNCONV_TILE_HALO_R128x256: 128, NNCONV_TILE_HALO_R224x256: 32}
+                  NNCONV_TILE_HALO_R128x256: 128, NNCONV_TILE_HALO_R224x256: 32,
+                  NNCONV_TILE_HALO_R256x64S: 128}
 # filter taps the halo tiles with register-held weights take (3x3 only)
 HALO_TILE_TAPS = {NNCONV_TILE_HALO_R256x128: 9, NNCONV_TILE_HALO_R128x256: 9,
-                  NNCONV_TILE_HALO_R224x256: 9}
+                  NNCONV_TILE_HALO_R224x256: 9, NNCONV_TILE_HALO_R256x64S: 9}
+# the pass's reduction channel count the single-slice halo tile requires
+HALO_TILE_RED = {NNCONV_TILE_HALO_R256x64S: 64}
 TILES = (NNCONV_TILE_256x256_8W, NNCONV_TILE_128x128_2S, NNCONV_TILE_128x128, NNCONV_TILE_128x64,
          NNCONV_TILE_256x256_16W, NNCONV_TILE_256x256_RING, NNCONV_TILE_256x128_RING,
          NNCONV_TILE_256x64_RING)

@@ -188,7 +188,7 @@ def test_forced_tile_validation(nnlib):
     calls = (nc.nnconv_fwd_tile, nc.nnconv_dgrad_tile)
     for f in calls:
         assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, -1) == inv
-        for bad in (5, 15, 99):  # block-diagonal tile, out of range
+        for bad in (5, 16, 99):  # block-diagonal tile, out of range
             assert f(dense, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, bad) == uns
         # 16 reduction channels per tap: not the 64-channel-slice kernel
         small = nc.make_desc(2, 16, 8, 8, 16, 3, 3, pad=(1, 1))
@@ -225,6 +225,13 @@ def test_forced_tile_validation(nnlib):
         wide = nc.make_desc(2, 64, 8, 32, 64, 3, 3, pad=(1, 1))
         assert f(wide, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None,
                  nc.NNCONV_TILE_HALO_R256x128) == uns
+    # the single-slice tile takes a reduction of 64 channels: C forward, K
+    # backward-data
+    c128 = nc.make_desc(2, 128, 8, 8, 64, 3, 3, pad=(1, 1))
+    k128 = nc.make_desc(2, 64, 8, 8, 128, 3, 3, pad=(1, 1))
+    single = nc.NNCONV_TILE_HALO_R256x64S
+    assert nc.nnconv_fwd_tile(c128, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, single) == uns
+    assert nc.nnconv_dgrad_tile(k128, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, single) == uns
 
 
 def test_noalloc_wgrad_validation(nnlib):

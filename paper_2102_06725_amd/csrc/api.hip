@@ -149,20 +149,29 @@ struct WgPlan {
 };
 
 // Backward-weight tile and workgroup target, from measurements on the
-// ResNet-50 layers at batch 256: 256x256 tiles and about 256 workgroups
-// (long pixel ranges, few partial tiles to write and reduce) when both GEMM
-// sides are at least 256 wide; 64-row tiles and more pixel splits (1024
-// workgroups) when Kg <= 64; otherwise 128x128 tiles and 512 workgroups,
-// single-stage for very wide filters (R*S*Cg >= 4096), where more resident
-// workgroups per CU pay off.
-WGConfig pick_wg(int64_t kg, int64_t rscg) {
+// ResNet-50 layers at batch 256:
+//   - 256x256 tiles and about 256 workgroups (long pixel ranges, few partial
+//     tiles to write and reduce) for filters of several taps when both GEMM
+//     sides are at least 256 wide;
+//   - 64-row tiles when Kg <= 64, with 1024 workgroups for filters of
+//     several taps and 512 for 1x1 ones (the 56x56 1x1 layers into 64
+//     channels: 37 / 99 us against 41 / 111 with 1024);
+//   - otherwise 128x128 tiles and 512 workgroups, single-stage for very wide
+//     filters (R*S*Cg >= 4096), where more resident workgroups per CU pay
+//     off.  This includes the 1x1 layers with both sides at least 256 wide,
+//     which read both operands once and are bound by memory traffic: there
+//     the 256x256 tiles' longer pixel ranges do not pay for the extra
+//     operand streams of half as many workgroups (14x14 and 7x7 1x1 layers:
+//     43 us against 49-51).
+WGConfig pick_wg(int64_t kg, int64_t rscg, int64_t taps) {
     if (kg <= 64) return WG_64x128;
-    if (kg >= 256 && rscg >= 256 && rscg < 4096) return WG_256x256;
+    if (taps > 1 && kg >= 256 && rscg >= 256 && rscg < 4096) return WG_256x256;
     return rscg >= 4096 ? WG_128x128S : WG_128x128;
 }
 
-int64_t wg_target_blocks(WGConfig cfg) {
-    return (cfg == WG_64x128 || cfg == WG_64x128D) ? 1024 : cfg == WG_256x256 ? 256 : 512;
+int64_t wg_target_blocks(WGConfig cfg, int64_t taps) {
+    if (cfg == WG_64x128 || cfg == WG_64x128D) return taps > 1 ? 1024 : 512;
+    return cfg == WG_256x256 ? 256 : 512;
 }
 
 WgPlan plan_wgrad_fast(const Geom &G) {
@@ -176,7 +185,7 @@ WgPlan plan_wgrad_fast(const Geom &G) {
         return pl;
     }
     const int64_t rscg = G.r * G.s * G.cg;
-    pl.cfg = pick_wg(G.kg, rscg);
+    pl.cfg = pick_wg(G.kg, rscg, G.r * G.s);
     if (G.diag32 && pl.cfg == WG_64x128 && G.kg == SUPER_GROUP) pl.cfg = WG_64x128D;
     static const int64_t tile_m[] = {128, 64, 256, 128, 64};
     static const int64_t tile_n[] = {128, 128, 256, 128, 128};
@@ -184,7 +193,7 @@ WgPlan plan_wgrad_fast(const Geom &G) {
     const int64_t tiles = G.g * ((G.kg + bmk - 1) / bmk) * ((rscg + bnj - 1) / bnj);
     const int64_t npq = G.n * G.p * G.q;
     const int64_t iters = (npq + 63) / 64;  // 64-pixel units
-    const int64_t target = wg_target_blocks(pl.cfg);
+    const int64_t target = wg_target_blocks(pl.cfg, G.r * G.s);
     int64_t splits = (target + tiles - 1) / tiles;
     int64_t max_splits = iters / 4;  // at least 256 pixels per split
     if (max_splits < 1) max_splits = 1;

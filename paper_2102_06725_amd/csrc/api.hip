@@ -142,11 +142,34 @@ bool stem_shape(const Geom &G) {
 // Stem backward-weight: persistent workgroups (one split-K partial each).
 constexpr int64_t STEM_WG_SPLITS = 256;
 
+int device_cus();
+
 struct WgPlan {
     bool stem;  // patch kernel (stem_shape)
     WGConfig cfg;
     int32_t splits, pix_per_split;
+    int32_t rb, blocks_per_img, nblocks, blocks_per_split;  // WG_HALO: row blocks
 };
+
+// Rows per block of the row-block backward-weight kernel (wgrad_halo.hip)
+// for this geometry, or 0 when it does not run it: 3x3 stride-1 "same"
+// convolutions (padding 1, dilation 1) of one group with 64 input and 64
+// output channels (not super-groups of smaller groups), on images whose
+// width admits blocks of whole rows of a multiple of 16 and at most 128
+// pixels (the largest such block is taken) that fits the kernel's LDS
+// buffers.
+int64_t wgh_rows(const Geom &G) {
+    if (!(G.g == 1 && !G.diag32 && G.cg == 64 && G.kg == 64 && G.r == 3 && G.s == 3 && G.sh == 1 &&
+          G.sw == 1 && G.dh == 1 && G.dw == 1 && G.ph == 1 && G.pw == 1 && G.p == G.h &&
+          G.q == G.w))
+        return 0;
+    int64_t rb0 = 1;
+    while ((rb0 * G.w) % 16 != 0) ++rb0;  // at most 16
+    if (rb0 * G.w > 128) return 0;
+    const int64_t rb = rb0 * (128 / (rb0 * G.w));
+    if (wgh_slots((int)rb, (int)G.w) > WGH_MAX_SLOTS) return 0;
+    return rb;
+}
 
 // Backward-weight tile and workgroup target, from measurements on the
 // ResNet-50 layers at batch 256:
@@ -175,12 +198,26 @@ int64_t wg_target_blocks(WGConfig cfg, int64_t taps) {
 }
 
 WgPlan plan_wgrad_fast(const Geom &G) {
-    WgPlan pl;
+    WgPlan pl = {};
     pl.stem = stem_shape(G);
     if (pl.stem) {
         const int64_t tiles = G.n * ((G.p + 15) / 16) * ((G.q + 15) / 16);
         pl.cfg = WG_128x128;
         pl.splits = (int32_t)(tiles < STEM_WG_SPLITS ? tiles : STEM_WG_SPLITS);
+        pl.pix_per_split = 0;
+        return pl;
+    }
+    pl.rb = (int32_t)wgh_rows(G);
+    if (pl.rb > 0) {
+        // one workgroup per CU, consecutive row blocks each
+        pl.cfg = WG_HALO;
+        pl.blocks_per_img = (int32_t)((G.h + pl.rb - 1) / pl.rb);
+        const int64_t nb = G.n * pl.blocks_per_img;
+        const int64_t cus = device_cus();
+        const int64_t per = (nb + cus - 1) / cus;
+        pl.nblocks = (int32_t)nb;
+        pl.blocks_per_split = (int32_t)per;
+        pl.splits = (int32_t)((nb + per - 1) / per);
         pl.pix_per_split = 0;
         return pl;
     }
@@ -751,6 +788,24 @@ nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *pa
         sp.ph = (int32_t)G.ph; sp.pw = (int32_t)G.pw;
         sp.alpha = 1.0f;
         TRY_HIP(launch_stem_wgrad(G.dtype, sp, part, pl.splits, st));
+        return NNCONV_OK;
+    }
+    if (pl.cfg == WG_HALO) {
+        WGHParams hp;
+        memset(&hp, 0, sizeof(hp));
+        hp.x = x;
+        hp.dy = dy;
+        hp.ws = part;
+        hp.x_bytes = (uint32_t)(G.n * G.h * G.w * G.c * 2);
+        hp.dy_bytes = (uint32_t)(G.n * G.p * G.q * G.k * 2);
+        hp.h = (int32_t)G.h; hp.w = (int32_t)G.w;
+        hp.c_stride = (int32_t)G.c; hp.k_stride = (int32_t)G.k;
+        hp.rb = pl.rb;
+        hp.blocks_per_img = pl.blocks_per_img;
+        hp.nblocks = pl.nblocks;
+        hp.blocks_per_split = pl.blocks_per_split;
+        hp.splits = pl.splits;
+        TRY_HIP(launch_wgrad_halo(G.dtype, hp, st));
         return NNCONV_OK;
     }
     WGParams p;

@@ -176,10 +176,30 @@ struct WGParams {
 };
 
 enum WGConfig { WG_128x128 = 0, WG_64x128 = 1, WG_256x256 = 2, WG_128x128S = 3,
-                WG_64x128D = 4 };  // WG_64x128 for block-diagonal super-group gradients
+                WG_64x128D = 4,  // WG_64x128 for block-diagonal super-group gradients
+                WG_HALO = 5 };   // wgrad_halo.hip (3x3 stride-1 "same", 64 -> 64 channels)
 
 // Pixel ranges of pix_per_split (a multiple of 32) pixels each.
 hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);
+
+// Backward-weight of a 3x3 stride-1 convolution with padding 1, one group,
+// 64 input and 64 output channels (wgrad_halo.hip): blocks of rb whole image
+// rows (rb * w a multiple of 16, at most 128 pixels, wgh_slots(rb, w) at
+// most WGH_MAX_SLOTS), blocks_per_split consecutive blocks per workgroup,
+// each workgroup writing ws[split][64][9 * 64] (fp32, columns (tap, c)).
+constexpr int WGH_MAX_SLOTS = 3392;
+// 16-byte LDS slots a block of rb rows of a w-wide image stages
+int wgh_slots(int rb, int w);
+struct WGHParams {
+    const void *x;
+    const void *dy;
+    float *ws;
+    uint32_t x_bytes, dy_bytes;
+    int32_t h, w;                  // image size (input = output)
+    int32_t c_stride, k_stride;    // channels per pixel of x and dy
+    int32_t rb, blocks_per_img, nblocks, blocks_per_split, splits;
+};
+hipError_t launch_wgrad_halo(int dtype, const WGHParams &p, hipStream_t st);
 
 // dw[e'] = (accumulate ? dw[e'] : 0) + inv_scale * sum_{s < splits} ws[s][e]
 // over e < count = K * R*S*Cg; e' = e for [K][R][S][Cg] output, or the

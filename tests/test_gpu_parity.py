@@ -65,6 +65,14 @@ SMALL = [
     ("3x3 bf16", Case(L("l", 3, 64, 11, 13, 72, 3, 3, 1, 1), dtype=I.BF16)),
     ("3x3 s2 bf16 NCHW", Case(L("m", 2, 32, 15, 14, 40, 3, 3, 2, 1), dtype=I.BF16, layout="nchw")),
     ("wgrad many splits", Case(L("n", 4, 64, 28, 28, 64, 3, 3, 1, 1))),
+    # 3x3 64 -> 64 backward-weight in blocks of whole image rows: blocks of
+    # 2 rows of 56, 8 of 14, 16 of 7 and 8 of 10 pixels; heights that leave
+    # a partial last block; several blocks per workgroup
+    ("row blocks W56", Case(L("rb1", 2, 64, 5, 56, 64, 3, 3, 1, 1))),
+    ("row blocks W14 bf16", Case(L("rb2", 3, 64, 13, 14, 64, 3, 3, 1, 1), dtype=I.BF16)),
+    ("row blocks W7", Case(L("rb3", 5, 64, 7, 7, 64, 3, 3, 1, 1))),
+    ("row blocks W10 NCHW", Case(L("rb4", 2, 64, 9, 10, 64, 3, 3, 1, 1), layout="nchw")),
+    ("row blocks many per split", Case(L("rb5", 300, 64, 4, 8, 64, 3, 3, 1, 1))),
     ("loss scale 1024", Case(L("o", 2, 64, 14, 14, 128, 3, 3, 1, 1), loss_scale=1024.0,
                              dy_std=1e-3)),
     ("direct: C3 unpadded", Case(L("p", 2, 3, 10, 10, 16, 3, 3, 1, 1))),

@@ -178,7 +178,7 @@ typedef enum {
  * tile; UNSUPPORTED when the tile is not one of nnconv_tile, or when the
  * call would not run on the implicit-GEMM kernel (reduction channels per tap
  * not a multiple of 64, depthwise or small-group convolution, the stem's
- * 8-channel shape, operands not 16-byte aligned or past 2 GiB, backward-data
+ * 8- and 4-channel shapes, operands not 16-byte aligned or past 2 GiB, backward-data
  * with more than 4 stride phases), and for a halo tile on any other geometry
  * than the one it states or on grouped convolution. */
 nnconv_status nnconv_fwd_tile(const nnconv_desc *desc, const void *x, const void *w, void *y,
@@ -234,13 +234,14 @@ nnconv_status nnconv_wgrad_noalloc(const nnconv_desc *desc, const void *x, const
  * read channel-last tensors, where one 16-byte load is 8 consecutive
  * channels of a pixel; these calls move data between the two forms (the
  * NCHW entry points above use them internally through the workspace) and
- * pad the channel count of the 3-channel input image to 8 for the stem.
+ * pad the channel count of the 3-channel input image to 4 (or 8) for the
+ * stem.
  * All pointers are caller-owned device memory; src and dst must not
  * overlap.  INVALID_ARG for null pointers or non-positive sizes (or a pad
  * below the channel count); MISALIGNED for pointers not 2-byte aligned.
  *
  * Activations: src[N][C][H][W] -> dst[N][H][W][c_pad], c_pad >= C; channels
- * C..c_pad-1 of dst are zero (the stem's 3 channels padded to 8). */
+ * C..c_pad-1 of dst are zero (the stem's 3 channels padded to 4). */
 nnconv_status nnconv_nchw_to_nhwc(const void *src, void *dst, int32_t n, int32_t c, int32_t h,
                                   int32_t w, int32_t c_pad, void *hip_stream);
 

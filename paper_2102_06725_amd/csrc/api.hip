@@ -133,10 +133,26 @@ C64Config pick_c64_geom(const Geom &G, int64_t m, int64_t ncols, int64_t red) {
 // planning: workspace regions and split counts (pure functions of the shape)
 // ---------------------------------------------------------------------------
 
-// 8-channel pixels into 64 channels with the stem's filter: the patch kernel.
+// 8-channel pixels into 64 channels with the stem's filter: the patch
+// kernel; 4-channel pixels too when the left padding is odd and the image
+// width even.
 bool stem_shape(const Geom &G) {
-    return G.cg == 8 && G.g == 1 && G.k == 64 && G.dh == 1 && G.dw == 1 &&
-           stem_fwd_supported((int)G.r, (int)G.s, (int)G.sh, (int)G.sw);
+    if (!(G.g == 1 && G.k == 64 && G.dh == 1 && G.dw == 1 &&
+          stem_fwd_supported((int)G.r, (int)G.s, (int)G.sh, (int)G.sw)))
+        return false;
+    return G.cg == 8 || (G.cg == 4 && G.pw % 2 == 1 && G.w % 2 == 0);
+}
+
+// Whether pass `pass` of this shape runs on the channel-last kernels: the
+// implicit-GEMM shapes, and the forward and backward-weight passes of the
+// 4-channel stem in channel-last layout (its backward-data and its NCHW
+// calls take the direct kernels).
+bool fast_pass(const Geom &G, nnconv_pass pass) {
+    if (fast_shape(G)) return true;
+    if (!(G.cg == 4 && stem_shape(G) && pass != NNCONV_DGRAD && G.layout == NNCONV_NHWC))
+        return false;
+    const int64_t lim = MAX_BUFFER_BYTES / 2;
+    return G.n * G.h * G.w * G.c <= lim && G.n * G.p * G.q * G.k <= lim;
 }
 
 // Stem backward-weight: persistent workgroups (one split-K partial each).
@@ -204,6 +220,7 @@ WgPlan plan_wgrad_fast(const Geom &G) {
         const int64_t tiles = G.n * ((G.p + 15) / 16) * ((G.q + 15) / 16);
         pl.cfg = WG_128x128;
         pl.splits = (int32_t)(tiles < STEM_WG_SPLITS ? tiles : STEM_WG_SPLITS);
+        if (G.cg == 4) pl.splits *= 2;  // two partials per workgroup
         pl.pix_per_split = 0;
         return pl;
     }
@@ -371,7 +388,7 @@ size_t workspace_bytes(const Geom &G, nnconv_pass pass) {
         return a > b ? a : b;
     }
     size_t d = direct_ws(G, pass);
-    if (!fast_shape(G)) return d;
+    if (!fast_pass(G, pass)) return d;
     size_t f = fast_regions(G, pass).total;
     return f > d ? f : d;
 }
@@ -599,6 +616,7 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
         sp.p = (int32_t)G.p; sp.q = (int32_t)G.q;
         sp.r = (int32_t)G.r; sp.s = (int32_t)G.s; sp.sh = (int32_t)G.sh; sp.sw = (int32_t)G.sw;
         sp.ph = (int32_t)G.ph; sp.pw = (int32_t)G.pw;
+        sp.c = (int32_t)G.c;
         sp.alpha = alpha;
         return hip_status(launch_stem_fwd(G.dtype, sp, device_cus(), st));
     }
@@ -786,6 +804,7 @@ nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *pa
         sp.p = (int32_t)G.p; sp.q = (int32_t)G.q;
         sp.r = (int32_t)G.r; sp.s = (int32_t)G.s; sp.sh = (int32_t)G.sh; sp.sw = (int32_t)G.sw;
         sp.ph = (int32_t)G.ph; sp.pw = (int32_t)G.pw;
+        sp.c = (int32_t)G.c;
         sp.alpha = 1.0f;
         TRY_HIP(launch_stem_wgrad(G.dtype, sp, part, pl.splits, st));
         return NNCONV_OK;
@@ -1054,7 +1073,7 @@ static nnconv_status fwd_impl(const nnconv_desc *desc, const void *x, const void
     if (sg_shape(G) && fast_shape(sg_geom(G)) && aligned(x, 16) && aligned(y, 16) &&
         aligned(ws, 16))
         return sg_fwd(G, x, w, y, alpha, (char *)ws, s);
-    const bool fast = fast_shape(G) && aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
+    const bool fast = fast_pass(G, NNCONV_FWD) && aligned(x, 16) && aligned(w, 16) && aligned(y, 16) &&
                       (G.layout == NNCONV_NHWC || aligned(ws, 16));
     if (!fast) return hip_status(launch_direct_fwd(G.dtype, direct_params(G, alpha), x, w, y, s));
     const Regions R = fast_regions(G, NNCONV_FWD);
@@ -1192,7 +1211,8 @@ static nnconv_status wgrad_run(const Geom &G, const void *x, const void *dy, voi
         aligned(ws, 16))
         return sg_wgrad(G, x, dy, dw, out_code, inv_loss_scale, accumulate, overflow_flag,
                         (char *)ws, s);
-    const bool fast = fast_shape(G) && aligned(x, 16) && aligned(dy, 16) && aligned(ws, 16);
+    const bool fast = fast_pass(G, NNCONV_WGRAD) && aligned(x, 16) && aligned(dy, 16) &&
+                      aligned(ws, 16);
     if (!fast) {
         const int32_t splits = plan_wgrad_direct_splits(G);
         float *part = (float *)ws;

@@ -551,10 +551,40 @@ __global__ __launch_bounds__(256) void pad_channels16_vec_kernel(const uint16_t 
     dst[i] = u32x4{v[0], v[1], v[2], v[3]};
 }
 
+// c_pad == 4 and dst 16-byte aligned: one thread builds two 4-channel
+// pixels (16 bytes; the last thread of an odd row count one, 8 bytes).
+__global__ __launch_bounds__(256) void pad_channels4_vec_kernel(const uint16_t *__restrict__ src,
+                                                                u32x4 *__restrict__ dst,
+                                                                int64_t rows, int32_t c) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t r0 = 2 * i;
+    if (r0 >= rows) return;
+    uint32_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int64_t row = r0 + (u >> 1);
+        const int a = 2 * (u & 1), b = a + 1;
+        const uint16_t *sp = src + row * c;
+        const uint32_t lo = row < rows && a < c ? sp[a] : 0u;
+        const uint32_t hi = row < rows && b < c ? sp[b] : 0u;
+        v[u] = lo | (hi << 16);
+    }
+    if (r0 + 1 < rows)
+        dst[i] = u32x4{v[0], v[1], v[2], v[3]};
+    else
+        *(u32x2 *)&dst[i] = u32x2{v[0], v[1]};
+}
+
 hipError_t launch_pad_channels16(const void *src, void *dst, int64_t rows, int32_t c,
                                  int32_t c_pad, hipStream_t st) {
     const int64_t total = rows * c_pad;
     if (total <= 0) return hipSuccess;
+    if (c_pad == 4 && ((uintptr_t)dst % 16) == 0) {
+        const int64_t pairs = (rows + 1) / 2;
+        hipLaunchKernelGGL(pad_channels4_vec_kernel, dim3((uint32_t)((pairs + 255) / 256)), dim3(256),
+                           0, st, (const uint16_t *)src, (u32x4 *)dst, rows, c);
+        return hipGetLastError();
+    }
     if (c_pad % 8 == 0 && ((uintptr_t)dst % 16) == 0) {
         const int64_t chunks = total / 8;
         hipLaunchKernelGGL(pad_channels16_vec_kernel, dim3((uint32_t)((chunks + 255) / 256)),

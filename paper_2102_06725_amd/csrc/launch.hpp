@@ -146,13 +146,18 @@ struct StemParams {
     uint32_t y_bytes;
     int32_t n, h, w, p, q;
     int32_t r, s, sh, sw, ph, pw;
+    int32_t c;                  // channels per pixel: 8, or 4 (stem4_supported)
     float alpha;
 };
 bool stem_fwd_supported(int r, int s, int sh, int sw);
+// 4-channel pixels: the same filter with an odd left padding and an even
+// image width
+bool stem4_supported(const StemParams &p);
 // cus: workgroups to launch at most (one per CU; the kernel loops over tiles)
 hipError_t launch_stem_fwd(int dtype, const StemParams &p, int cus, hipStream_t st);
 // Backward-weight partials for the same shapes: y holds dy; splits
-// workgroups each write part[split][64][r*s*8] (no loss-scale step).
+// workgroups each write part[split][64][r*s*c] (no loss-scale step); with
+// 4-channel pixels splits is even and splits / 2 workgroups write two each.
 hipError_t launch_stem_wgrad(int dtype, const StemParams &p, float *part, int splits,
                              hipStream_t st);
 

@@ -103,7 +103,7 @@ class Layer:
     pad: int = 0
     dil: int = 1
     groups: int = 1
-    c_logical: int = 0      # channel count before padding (stem: 3 padded to 8)
+    c_logical: int = 0      # channel count before padding (stem: 3 padded to 4)
     count: int = 1          # how many ResNet-50 layers share this shape
     dgrad: bool = True      # the stem has no gradient to the image
     # width-axis stride / padding / dilation when they differ from the
@@ -149,11 +149,11 @@ class Layer:
 def resnet50_layers(batch: int) -> List[Tuple[Layer, int]]:
     """ResNet-50 v1.5 (stride on the 3x3 conv of each down-sampling block):
     the 23 distinct convolution shapes with their multiplicities (sum 53).
-    The stem's 3 input channels are padded to 8."""
+    The stem's 3 input channels are padded to 4."""
     L = []
     def add(name, c, h, k, r, stride, pad, count, **kw):
         L.append(Layer(name, batch, c, h, h, k, r, r, stride, pad, count=count, **kw))
-    add("stem", 8, 224, 64, 7, 2, 3, 1, c_logical=3, dgrad=False)
+    add("stem", 4, 224, 64, 7, 2, 3, 1, c_logical=3, dgrad=False)
     add("s2b0a", 64, 56, 64, 1, 1, 0, 1)
     add("s2b0b", 64, 56, 64, 3, 1, 1, 3)
     add("s2b0c", 64, 56, 256, 1, 1, 0, 4)
@@ -262,7 +262,7 @@ def workload(cfg: int, dtype: str = F16, batch: int | None = None) -> Workload:
                         1024.0, "absnormal", 1.0, "he", 1e-3)
     if cfg == 4:
         n = batch or 128
-        ls = (Layer("stem 7x7 3(8)->64 s2", n, 8, 224, 224, 64, 7, 7, 2, 3, c_logical=3,
+        ls = (Layer("stem 7x7 3(4)->64 s2", n, 4, 224, 224, 64, 7, 7, 2, 3, c_logical=3,
                     dgrad=False),)
         return Workload("ResNet-50 stem batch %d" % n, ls, "nhwc", dtype, 1024.0,
                         "normal", 1.0, "he", 1e-3, passes=("fwd", "wgrad"))

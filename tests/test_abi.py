@@ -202,7 +202,7 @@ def test_forced_tile_validation(nnlib):
         assert f(dense, FAKE + 2, FAKE + 2, FAKE + 2, 1.0, FAKE, 1 << 30, None, 2) == uns
         # still the ordinary checks first
         assert f(dense, None, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == inv
-    # the stem's 8-channel shape has its own forward kernel
+    # the stem's 8-channel shape has its own forward kernel (as has the 4-channel one)
     stem = nc.make_desc(2, 8, 32, 32, 64, 7, 7, stride=(2, 2), pad=(3, 3))
     assert nc.nnconv_fwd_tile(stem, FAKE, FAKE, FAKE, 1.0, FAKE, 1 << 30, None, 2) == uns
     # backward-data with more than four stride phases

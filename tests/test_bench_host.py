@@ -27,9 +27,9 @@ def test_forward_launch_classifier():
     # launch order of two sweep layers and a depthwise layer, as bench.py queues them
     names = [
         "at::native::FillFunctor",                                    # flag clear
-        "nnconv::pad_channels16_vec_kernel",                          # stem padding
-        "nnconv::stem_fwd_kernel<nnconv::Half, 7, 7, 2, 2>",          # fwd
-        "nnconv::stem_wgrad_kernel<nnconv::Half, 7, 7, 2, 2>",
+        "nnconv::pad_channels4_vec_kernel",                           # stem padding
+        "nnconv::stem_fwd4_kernel<nnconv::Half>",                     # fwd
+        "nnconv::stem_wgrad4_kernel<nnconv::Half>",
         "nnconv::wgrad_reduce_vec_kernel<2, 16>",
         "nnconv::igemm_c64_kernel<nnconv::Half, 128, 64, 2, 2, 8, 1, false, false>",  # fwd
         "nnconv::transpose16_vec_kernel",

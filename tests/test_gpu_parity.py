@@ -56,6 +56,14 @@ SMALL = [
     ("1x1 K512 many n-tiles", Case(L("d2", 2, 128, 5, 6, 512, 1, 1))),
     ("stem-like 7x7 s2 C3 padded to 8", Case(L("e", 2, 8, 23, 21, 64, 7, 7, 2, 3, c_logical=3),
                                             x_kind="normal")),
+    # 4-channel stem pixels: partial tiles, all four channels live, bf16, and
+    # an odd width (the direct kernels)
+    ("stem-like C3 padded to 4", Case(L("e4", 2, 4, 24, 22, 64, 7, 7, 2, 3, c_logical=3),
+                                      x_kind="normal")),
+    ("stem-like C4 2x2 tiles", Case(L("e5", 3, 4, 40, 36, 64, 7, 7, 2, 3), x_kind="normal")),
+    ("stem-like C3(4) bf16", Case(L("e6", 2, 4, 34, 50, 64, 7, 7, 2, 3, c_logical=3),
+                                  x_kind="normal", dtype=I.BF16)),
+    ("stem-like C4 odd width", Case(L("e7", 2, 4, 15, 15, 64, 7, 7, 2, 3), x_kind="normal")),
     ("dilation 2", Case(L("f", 2, 16, 12, 12, 24, 3, 3, 1, 2, dil=2))),
     ("groups 2", Case(L("g", 2, 32, 9, 9, 48, 3, 3, 1, 1, groups=2))),
     ("5x5 stride 3 pad 2", Case(L("h", 1, 24, 17, 19, 16, 5, 5, 3, 2))),

@@ -61,7 +61,7 @@ def test_resnet50_has_53_layers():
 def test_workload_tensors_layout_and_padding():
     wl = I.workload(4, batch=1)
     t = I.layer_tensors(wl, 0, 4)
-    assert t["x"].shape == (1, 224, 224, 8)
+    assert t["x"].shape == (1, 224, 224, 4)
     assert not t["x"][..., 3:].any() and not t["w"][..., 3:].any()
     wl1 = I.workload(1)
     t1 = I.layer_tensors(wl1, 0, 1)

@@ -897,7 +897,7 @@ def main():
             traffic = stored_traffic("hbm") if args.workload == "sweep" and not args.layers \
                 and not args.batch and args.dtype == "f16" else None
             kern = "depthwise forward (dwt_fwd_kernel)" if depthwise else \
-                "forward implicit GEMM (igemm_c64_kernel; stem_fwd_kernel for the stem)"
+                "forward implicit GEMM (igemm_c64_kernel; stem_fwd4_kernel for the stem)"
             roofline_hbm = {"kernel": "%s, the %d layers of the workload whose forward pass is "
                                       "HBM-bound" % (kern, len(hb)),
                             "bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,

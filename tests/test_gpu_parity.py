@@ -64,6 +64,9 @@ SMALL = [
     ("stem-like C3(4) bf16", Case(L("e6", 2, 4, 34, 50, 64, 7, 7, 2, 3, c_logical=3),
                                   x_kind="normal", dtype=I.BF16)),
     ("stem-like C4 odd width", Case(L("e7", 2, 4, 15, 15, 64, 7, 7, 2, 3), x_kind="normal")),
+    ("stem-like C4 small odd height", Case(L("e8", 1, 4, 9, 8, 64, 7, 7, 2, 3), x_kind="normal")),
+    ("stem-like C4 padding 2 (direct)", Case(L("e9", 2, 4, 12, 14, 64, 7, 7, 2, 2),
+                                            x_kind="normal")),
     ("dilation 2", Case(L("f", 2, 16, 12, 12, 24, 3, 3, 1, 2, dil=2))),
     ("groups 2", Case(L("g", 2, 32, 9, 9, 48, 3, 3, 1, 1, groups=2))),
     ("5x5 stride 3 pad 2", Case(L("h", 1, 24, 17, 19, 16, 5, 5, 3, 2))),
@@ -81,6 +84,11 @@ SMALL = [
     ("row blocks W7", Case(L("rb3", 5, 64, 7, 7, 64, 3, 3, 1, 1))),
     ("row blocks W10 NCHW", Case(L("rb4", 2, 64, 9, 10, 64, 3, 3, 1, 1), layout="nchw")),
     ("row blocks many per split", Case(L("rb5", 300, 64, 4, 8, 64, 3, 3, 1, 1))),
+    ("row blocks W12 one row", Case(L("rb6", 3, 64, 1, 12, 64, 3, 3, 1, 1))),
+    ("row blocks W3", Case(L("rb7", 4, 64, 9, 3, 64, 3, 3, 1, 1))),
+    ("row blocks W1 (split-K instead)", Case(L("rb8", 4, 64, 7, 1, 64, 3, 3, 1, 1))),
+    ("row blocks W28 bf16 loss scale 1024", Case(L("rb9", 2, 64, 11, 28, 64, 3, 3, 1, 1),
+                                                  dtype=I.BF16, loss_scale=1024.0, dy_std=1e-3)),
     ("loss scale 1024", Case(L("o", 2, 64, 14, 14, 128, 3, 3, 1, 1), loss_scale=1024.0,
                              dy_std=1e-3)),
     ("direct: C3 unpadded", Case(L("p", 2, 3, 10, 10, 16, 3, 3, 1, 1))),

@@ -424,9 +424,13 @@ def summarize_profile(args):
 
         def occupancy(res):
             """Waves per SIMD allowed by registers (512 per lane, granule 8)
-            and by LDS (160 KiB per CU, 4 SIMDs)."""
+            and by LDS (160 KiB per CU, 4 SIMDs).  On gfx950 the trace's
+            VGPR_Count is half the registers a wave is given: the kernels
+            here, compiled with -Rpass-analysis=kernel-resource-usage, report
+            VGPRs + AGPRs (each rounded up to 8) equal to twice the trace's
+            count, and the occupancy that gives."""
             vg, ag, lds, wg = res
-            regs = ((vg + 7) // 8) * 8 + ((ag + 7) // 8) * 8
+            regs = ((2 * vg + 7) // 8) * 8 + ((ag + 7) // 8) * 8
             by_regs = min(8, 512 // max(8, regs))
             waves = max(1, wg // 64)
             by_lds = 8 if lds == 0 else (163840 // lds) * waves / 4.0
@@ -439,8 +443,9 @@ def summarize_profile(args):
             dur = sum(d["dur"] for d in ds) / len(ds)
             res = ds[0]["res"]
             occ = occupancy(res)
-            out.append("%s  n=%d  avg %.2f us  vgpr %d agpr %d lds %d wg %d  waves/SIMD: regs %d, "
-                       "lds %.1f" % ((name[:100], len(ds), dur / 1e3) + res + occ))
+            out.append("%s  n=%d  avg %.2f us  registers %d (trace vgpr %d agpr %d) lds %d wg %d  "
+                       "waves/SIMD: regs %d, lds %.1f"
+                       % ((name[:100], len(ds), dur / 1e3, 2 * res[0]) + res + occ))
             out.append("    " + "  ".join("%s=%.4g" % kv for kv in sorted(avg.items())))
             f = derived(avg, dur)
             if f:

@@ -274,15 +274,16 @@ struct Regions {  // byte offsets into the caller's workspace
 
 // Bytes of fragment-packed weights the register-weight halo tiles need for
 // this geometry and pass: 3x3 filters, stride 1, output the input's size,
-// one group, 64-channel multiples, taps within the larger halo buffer's
-// span.  0 when no such tile can run it.
+// 64-channel multiples, taps within the larger halo buffer's span, and one
+// group or groups of 64 channels (the single-slice tile).  0 when no such
+// tile can run it.
 size_t hring_ws(const Geom &G, nnconv_pass pass) {
-    if (!(G.g == 1 && G.sh == 1 && G.sw == 1 && G.p == G.h && G.q == G.w &&
-          G.r * G.s == HRING_TAPS && G.cg % 64 == 0 && G.kg % 64 == 0 &&
+    if (!((G.g == 1 || (G.cg == 64 && G.kg == 64)) && G.sh == 1 && G.sw == 1 && G.p == G.h &&
+          G.q == G.w && G.r * G.s == HRING_TAPS && G.cg % 64 == 0 && G.kg % 64 == 0 &&
           (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw <= HALO_SPAN))
         return 0;
-    if (pass == NNCONV_FWD) return hring_pack_bytes(G.kg, G.cg);
-    if (pass == NNCONV_DGRAD) return hring_pack_bytes(G.cg, G.kg);
+    if (pass == NNCONV_FWD) return hring_pack_bytes(G.kg, G.cg, G.g);
+    if (pass == NNCONV_DGRAD) return hring_pack_bytes(G.cg, G.kg, G.g);
     return 0;
 }
 
@@ -514,14 +515,17 @@ bool hring_cfg(int hc) { return hring_config(hc); }
 
 // Whether the halo-staged kernel can run this shape's forward and
 // backward-data passes (the geometry halo_supported() accepts, stated on the
-// convolution): one group, stride 1, output the input's size, 64-channel
-// multiples, taps spanning at most HALO_SPAN raster positions.  `red` is the
+// convolution): one group (or, on the single-slice tile, groups of 64
+// channels), stride 1, output the input's size, 64-channel multiples, taps
+// spanning at most HALO_SPAN raster positions.  `red` is the
 // pass's reduction channel count (Cg forward, Kg backward-data), which the
 // single-slice tile needs to be 64.
 bool halo_geom(const Geom &G, int tile, int64_t red) {
     const HaloConfig hc = (HaloConfig)(tile - HALO_TILE0);
     const bool regw = hring_cfg(hc);
-    return G.g == 1 && G.sh == 1 && G.sw == 1 && G.p == G.h && G.q == G.w && G.cg % 64 == 0 &&
+    // one group, or groups of 64 channels on the single-slice tile
+    return (G.g == 1 || (hc == HALO_R256x64S && G.cg == 64 && G.kg == 64)) && G.sh == 1 &&
+           G.sw == 1 && G.p == G.h && G.q == G.w && G.cg % 64 == 0 &&
            G.kg % 64 == 0 && G.r * G.s <= 32 && (!regw || G.r * G.s == HRING_TAPS) &&
            (hc != HALO_R256x64S || red == 64) &&
            (G.r - 1) * G.dh * G.w + (G.s - 1) * G.dw <= halo_cfg_span(hc);
@@ -550,6 +554,12 @@ bool halo_geom(const Geom &G, int tile, int64_t red) {
 // than the 64-channel-slice ones (40-60% on the 7x7 1x1 layers).
 int device_cus();
 int pick_halo(const TNParams &p, bool pack) {
+    // groups of 64 channels (super-groups of a grouped convolution): the
+    // single-slice tile or none
+    if (p.groups > 1)
+        return pack && p.ph[0].tap_count == HRING_TAPS && halo_cfg_supported(p, HALO_R256x64S)
+                   ? HALO_R256x64S
+                   : -1;
     if (p.ph[0].tap_count < 2 || !halo_supported(p)) return -1;
     if (pack && p.ph[0].tap_count == HRING_TAPS) {
         if (p.cr == 64 && p.ncols <= 64 && halo_cfg_supported(p, HALO_R256x64S))
@@ -671,7 +681,8 @@ nnconv_status fwd_fast(const Geom &G, const void *x, const void *w, void *y, flo
         if (hc >= 0) {
             if (!halo_cfg_supported(p, (HaloConfig)hc) || (hring_cfg(hc) && !pack))
                 return NNCONV_ERR_UNSUPPORTED;
-            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, pack, st));
+            return hip_status(
+                launch_igemm_halo(G.dtype, (HaloConfig)hc, p, pack, G.diag32 != 0, st));
         }
         const C64Config cfg =
             tile >= 0 ? (C64Config)tile : pick_c64_geom(G, p.M, G.kg, (int64_t)t * G.cg);
@@ -751,7 +762,8 @@ nnconv_status dgrad_fast(const Geom &G, const void *dy, const void *wt, void *dx
         if (hc >= 0) {
             if (!halo_cfg_supported(p, (HaloConfig)hc) || (hring_cfg(hc) && !pack))
                 return NNCONV_ERR_UNSUPPORTED;
-            return hip_status(launch_igemm_halo(G.dtype, (HaloConfig)hc, p, pack, st));
+            return hip_status(
+                launch_igemm_halo(G.dtype, (HaloConfig)hc, p, pack, G.diag32 != 0, st));
         }
         const C64Config cfg =
             tile >= 0 ? (C64Config)tile : pick_c64_geom(G, rows, G.cg, red_rows / rows);
@@ -939,10 +951,11 @@ nnconv_status sg_fwd(const Geom &G, const void *x, const void *w, void *y, float
     void *wexp = ws + R.d;
     TRY_HIP(launch_expand_group_weights(w, wexp, G.k, (int32_t)(G.r * G.s), (int32_t)G.cg,
                                         (int32_t)SUPER_GROUP, G.layout == NNCONV_NCHW, st));
-    if (G.layout == NNCONV_NHWC) return fwd_fast(S, x, wexp, y, alpha, st);
+    void *pack = hring_ws(S, NNCONV_FWD) > 0 ? ws + R.f : nullptr;
+    if (G.layout == NNCONV_NHWC) return fwd_fast(S, x, wexp, y, alpha, st, -1, pack);
     void *xt = ws + R.a, *yt = ws + R.c;
     TRY_HIP(launch_transpose16(x, xt, G.n, G.c, G.h * G.w, G.c, st));
-    nnconv_status s = fwd_fast(S, xt, wexp, yt, alpha, st);
+    nnconv_status s = fwd_fast(S, xt, wexp, yt, alpha, st, -1, pack);
     if (s != NNCONV_OK) return s;
     return hip_status(launch_transpose16(yt, y, G.n, G.p * G.q, G.k, G.p * G.q, st));
 }
@@ -956,10 +969,11 @@ nnconv_status sg_dgrad(const Geom &G, const void *dy, const void *w, void *dx, f
                                         (int32_t)SUPER_GROUP, G.layout == NNCONV_NCHW, st));
     // [g][Kg][R*S*Cg] -> [g][R*S*Cg][Kg] for the super-groups
     TRY_HIP(launch_transpose16(wexp, wt, S.g, S.kg, S.r * S.s * S.cg, S.kg, st));
-    if (G.layout == NNCONV_NHWC) return dgrad_fast(S, dy, wt, dx, alpha, st);
+    void *pack = hring_ws(S, NNCONV_DGRAD) > 0 ? ws + R.f : nullptr;
+    if (G.layout == NNCONV_NHWC) return dgrad_fast(S, dy, wt, dx, alpha, st, -1, pack);
     void *dyt = ws + R.a, *dxt = ws + R.c;
     TRY_HIP(launch_transpose16(dy, dyt, G.n, G.k, G.p * G.q, G.k, st));
-    nnconv_status s = dgrad_fast(S, dyt, wt, dxt, alpha, st);
+    nnconv_status s = dgrad_fast(S, dyt, wt, dxt, alpha, st, -1, pack);
     if (s != NNCONV_OK) return s;
     return hip_status(launch_transpose16(dxt, dx, G.n, G.h * G.w, G.c, G.h * G.w, st));
 }

@@ -295,8 +295,12 @@ int halo_tap_span(const TNParams &p) {
     return span > 0x7FFFFFFF ? 0x7FFFFFFF : (int)span;
 }
 
-bool halo_supported(const TNParams &p) {
-    if (p.nphase != 1 || p.groups != 1 || p.cr <= 0 || p.cr % 64 != 0 || p.a_c != p.cr)
+bool halo_supported(const TNParams &p, bool grouped) {
+    if (p.nphase != 1 || p.groups < 1 || p.cr <= 0 || p.cr % 64 != 0) return false;
+    if (p.groups == 1 ? p.a_c != p.cr
+                      : !grouped || (int64_t)p.a_c != (int64_t)p.groups * p.cr ||
+                            p.a_cg_ofs != p.cr || (int64_t)p.o_c != (int64_t)p.groups * p.ncols ||
+                            p.o_cg_ofs != p.ncols)
         return false;
     const TNPhase &F = p.ph[0];
     if (p.ai_mul != 1 || p.aj_mul != 1 || p.oi_mul != 1 || p.oj_mul != 1 || F.oi_add != 0 ||
@@ -311,13 +315,18 @@ int halo_cfg_span(HaloConfig cfg) {
 }
 
 bool halo_cfg_supported(const TNParams &p, HaloConfig cfg) {
-    if (hring_config(cfg))
-        return hring_supported(p, halo_cfg_span(cfg)) && (cfg != HALO_R256x64S || p.cr == 64);
+    // the single-slice tile takes groups of 64 reduction channels into 64
+    // output columns; every other configuration one group
+    if (cfg == HALO_R256x64S)
+        return hring_supported(p, halo_cfg_span(cfg), true) && p.cr == 64 &&
+               (p.groups == 1 || p.ncols == 64);
+    if (hring_config(cfg)) return hring_supported(p, halo_cfg_span(cfg));
     return halo_supported(p);
 }
 
-hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, hipStream_t st) {
-    if (hring_config(cfg)) return launch_igemm_hring(dtype, cfg, p, pack, st);
+hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, bool diag32,
+                             hipStream_t st) {
+    if (hring_config(cfg)) return launch_igemm_hring(dtype, cfg, p, pack, diag32, st);
     if (dtype == Half::id) return launch_halo_t<Half>(cfg, p, st);
     return launch_halo_t<BFloat>(cfg, p, st);
 }

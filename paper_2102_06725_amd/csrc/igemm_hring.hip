@@ -47,8 +47,14 @@ constexpr int KS = 4;   // 16-deep k-steps per 64-channel slice
 // 2 (double-buffered slices, one workgroup per CU), or 1 for a reduction of
 // a single 64-channel slice (the host checks cr == 64), where a tile stages
 // its halo once and OCC workgroups share a CU, one's staging and output
-// stage covered by the others' matrix-core work.
-template <class T, int BM, int BN, int WM, int WN, int HR, int NT, int D, int NB, int OCC>
+// stage covered by the others' matrix-core work.  The single-slice tile also
+// runs P.groups > 1 groups of 64 channels (super-groups of a grouped
+// convolution), each its own GEMM; DIAG: their 64x64 weight blocks are
+// block-diagonal in 32x32 blocks, so a 32-column block of a wave meets only
+// the matching 32 channels (two of the four k-steps) and the others are
+// neither loaded nor multiplied.
+template <class T, int BM, int BN, int WM, int WN, int HR, int NT, int D, int NB, int OCC,
+          bool DIAG = false>
 __global__ __launch_bounds__(WM * WN * 64, OCC)
 void igemm_hring_kernel(const TNParams P) {
     using namespace hring;
@@ -59,6 +65,7 @@ void igemm_hring_kernel(const TNParams P) {
     constexpr int H_SLOTS = HR * BKC;
     constexpr int ZERO = NB * H_SLOTS;     // one row of zeros
     static_assert(NB == 1 || NB == 2, "halo buffers");
+    static_assert(!DIAG || (NB == 1 && BN == 64), "block-diagonal: single-slice 64-column tile");
     // the output stage reuses the LDS for the BM x BN tile, which can be
     // larger than the two halo buffers
     constexpr int LDS_SLOTS = ZERO + BKC > BM * BN / 8 ? ZERO + BKC : BM * BN / 8;
@@ -75,11 +82,14 @@ void igemm_hring_kernel(const TNParams P) {
     const int l32 = lane & 31, khalf = lane >> 5;
 
     const TNPhase &F = P.ph[0];
-    // column tile outer: the workgroups of one XCD (consecutive local ids)
-    // share the column tile's packed weights in that XCD's L2
+    // group, then column tile outer: the workgroups of one XCD (consecutive
+    // local ids) share the column tile's packed weights in that XCD's L2
     const int local = (int)xcd_remap(blockIdx.x, gridDim.x);
-    const int tn = local / F.tiles_m;
-    const int tm = local - tn * F.tiles_m;
+    const int per_g = F.tiles_m * P.tiles_n;
+    const int g = local / per_g;
+    const int rem = local - g * per_g;
+    const int tn = rem / F.tiles_m;
+    const int tm = rem - tn * F.tiles_m;
     const int m0 = tm * BM, n0 = tn * BN;
     constexpr int ntaps = NT;  // the host checks F.tap_count == NT
     const int nslices = P.cr / 64;
@@ -129,15 +139,21 @@ void igemm_hring_kernel(const TNParams P) {
         const int r = (wave * H_LD + j) * RPI + lrow;
         const int p = m0 + lo + r;  // A pixel (raster index) of halo row r
         h_goff[j] = (r < hrows && p >= 0 && p < F.M)
-                        ? (uint32_t)p * (uint32_t)P.a_c * 2u + (uint32_t)lch * 16u
+                        ? ((uint32_t)p * (uint32_t)P.a_c + (uint32_t)(g * P.a_cg_ofs)) * 2u +
+                              (uint32_t)lch * 16u
                         : OOB_OFFSET;
         h_loff[j] = (uint32_t)(r * 128 + ((lch ^ ((r >> 1) & 7)) << 4));
     }
-    // Packed weights: fragment (slice c, tap t, column block cb, k-step ks)
-    // is the kilobyte at (((c * NT + t) * ncb + cb) * KS + ks) * 1024, lane
-    // l's 16 bytes at l * 16.  B fragment j of this wave is column block
-    // (n0 + wn * WTN) / 32 + j.
+    // Packed weights: fragment (group, slice c, tap t, column block cb,
+    // k-step ks) is the kilobyte at ((((group * nslices + c) * NT + t) * ncb +
+    // cb) * KS + ks) * 1024, lane l's 16 bytes at l * 16.  B fragment j of
+    // this wave is column block (n0 + wn * WTN) / 32 + j.
     const int ncb = (P.ncols + 31) / 32;
+    const uint32_t b_gshift = (uint32_t)(g * nslices * NT * ncb) * (uint32_t)(KS * 1024);
+    // DIAG: whether k-step ks meets column block j of this wave
+    auto live_block = [&](int ks, int j) {
+        return !DIAG || (ks >> 1) == (((wn * WTN) >> 5) + j) % 2;
+    };
     uint32_t b_goff[FN];
 #pragma unroll
     for (int j = 0; j < FN; ++j)
@@ -184,13 +200,15 @@ void igemm_hring_kernel(const TNParams P) {
     // the weight fragments of step (tap t, slice c) into ring entry e; past
     // the last step (live = false) nothing is read (zeros)
     auto load_b = [&](int t, int c, bool live, u32x4 (&e)[KS][FN]) {
-        const uint32_t shift = (uint32_t)((c * NT + t) * ncb) * (uint32_t)(KS * 1024);
+        const uint32_t shift =
+            b_gshift + (uint32_t)((c * NT + t) * ncb) * (uint32_t)(KS * 1024);
         const __amdgpu_buffer_rsrc_t r =
             rsrc(b_ptr + shift, (live && b_bytes > shift) ? b_bytes - shift : 0u);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-            for (int j = 0; j < FN; ++j) e[ks][j] = load16(r, b_goff[j] + (uint32_t)ks * 1024u);
+            for (int j = 0; j < FN; ++j)
+                if (live_block(ks, j)) e[ks][j] = load16(r, b_goff[j] + (uint32_t)ks * 1024u);
     };
 
     f32x16 acc[FN][FM];
@@ -218,11 +236,12 @@ void igemm_hring_kernel(const TNParams P) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) fa[i] = *(const u32x4 *)(lbase + (aa[i] ^ kx));
     };
-    auto mma = [&](const u32x4 (&fa)[FM], const u32x4 (&fb)[FN]) {
+    auto mma = [&](const u32x4 (&fa)[FM], const u32x4 (&fb)[FN], int ks) {
 #pragma unroll
         for (int j = 0; j < FN; ++j)
+            if (live_block(ks, j))
 #pragma unroll
-            for (int i = 0; i < FM; ++i) acc[j][i] = mfma32<T>(fb[j], fa[i], acc[j][i]);
+                for (int i = 0; i < FM; ++i) acc[j][i] = mfma32<T>(fb[j], fa[i], acc[j][i]);
     };
 
     // ---- prologue: zero row, halo of slice 0, weights of steps 0 .. D-1
@@ -259,7 +278,7 @@ void igemm_hring_kernel(const TNParams P) {
                 else
                     read_a(aa1, 0, fa[nxt]);
                 __builtin_amdgcn_sched_barrier(0);
-                mma(fa[cur], fbr[t % D][ks]);
+                mma(fa[cur], fbr[t % D][ks], ks);
                 __builtin_amdgcn_sched_barrier(0);
             }
             // ring entry t % D is free: the weights of step k + D
@@ -276,45 +295,49 @@ void igemm_hring_kernel(const TNParams P) {
         }
     }
 
-    store_tile<T, BM, BN, WM, WN, FM, FN>(acc, &lds[0], P, F, m0, n0, 0);
+    store_tile<T, BM, BN, WM, WN, FM, FN>(acc, &lds[0], P, F, m0, n0, g);
 }
 
-// Packs the B operand of a single-phase implicit GEMM (row `col`, tap t,
-// reduction channel ch at element col * b_ld + boff[t] + ch of p.b) into the
-// fragment order igemm_hring_kernel reads: 16 bytes per thread,
-// dst[(((c * ntaps + t) * ncb + cb) * 4 + ks) * 64 + l] = the 8 channels
-// c * 64 + ks * 16 + (l / 32) * 8 .. +7 of column cb * 32 + l % 32 (zeros
-// past ncols).
+// Packs the B operand of a single-phase implicit GEMM (group gr, row `col`,
+// tap t, reduction channel ch at element gr * b_g_ofs + col * b_ld + boff[t]
+// + ch of p.b) into the fragment order igemm_hring_kernel reads: 16 bytes per
+// thread, dst[((((gr * nslices + c) * ntaps + t) * ncb + cb) * 4 + ks) * 64 +
+// l] = the 8 channels c * 64 + ks * 16 + (l / 32) * 8 .. +7 of column
+// cb * 32 + l % 32 (zeros past ncols).
 __global__ __launch_bounds__(256)
 void pack_hring_b_kernel(const TNParams P, u32x4 *dst, int32_t total) {
-    const int g = (int)(blockIdx.x * 256 + threadIdx.x);
-    if (g >= total) return;
+    const int e = (int)(blockIdx.x * 256 + threadIdx.x);
+    if (e >= total) return;
     const int ntaps = P.ph[0].tap_count;
     const int ncb = (P.ncols + 31) / 32;
-    const int l = g & 63;
-    int f = g >> 6;
+    const int nslices = P.cr / 64;
+    const int l = e & 63;
+    int f = e >> 6;
     const int ks = f & 3;
     f >>= 2;
     const int cb = f % ncb;
     f /= ncb;
     const int t = f % ntaps;
-    const int c = f / ntaps;
+    f /= ntaps;
+    const int c = f % nslices;
+    const int gr = f / nslices;
     const int col = cb * 32 + (l & 31);
     const int ch = c * 64 + ks * 16 + (l >> 5) * 8;
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (col < P.ncols) {
         const __amdgpu_buffer_rsrc_t r = make_rsrc(P.b, P.b_bytes);
-        v = load16(r, (uint32_t)(col * P.b_ld + P.taps.boff[t] + ch) * 2u);
+        v = load16(r, (uint32_t)(gr * P.b_g_ofs + col * P.b_ld + P.taps.boff[t] + ch) * 2u);
     }
-    dst[g] = v;
+    dst[e] = v;
 }
 
-size_t hring_pack_bytes(int64_t ncols, int64_t cr) {
-    return (size_t)HRING_TAPS * (size_t)(cr / 64) * (size_t)((ncols + 31) / 32) * 4096u;
+size_t hring_pack_bytes(int64_t ncols, int64_t cr, int64_t groups) {
+    return (size_t)groups * (size_t)HRING_TAPS * (size_t)(cr / 64) *
+           (size_t)((ncols + 31) / 32) * 4096u;
 }
 
 hipError_t launch_hring_pack(const TNParams &p, void *dst, hipStream_t st) {
-    const int64_t total = (int64_t)hring_pack_bytes(p.ncols, p.cr) / 16;
+    const int64_t total = (int64_t)hring_pack_bytes(p.ncols, p.cr, p.groups) / 16;
     if (total <= 0) return hipSuccess;
     if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
     hipLaunchKernelGGL(pack_hring_b_kernel, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st,
@@ -325,16 +348,28 @@ hipError_t launch_hring_pack(const TNParams &p, void *dst, hipStream_t st) {
 namespace {
 
 template <class T, int BM, int BN, int WM, int WN, int HR, int NB = 2, int OCC = 1>
-hipError_t launch_hring_cfg(TNParams &p, hipStream_t st) {
-    if (!hring_supported(p, HR - BM) || (NB == 1 && p.cr != 64)) return hipErrorInvalidValue;
+hipError_t launch_hring_cfg(TNParams &p, bool diag32, hipStream_t st) {
+    // groups (of 64 channels into 64 columns) and block-diagonal weights on
+    // the single-slice tile only
+    constexpr bool SINGLE = NB == 1 && BN == 64;
+    if (!hring_supported(p, HR - BM, SINGLE) || (NB == 1 && p.cr != 64) ||
+        (p.groups > 1 && p.ncols != 64))
+        return hipErrorInvalidValue;
     p.tiles_n = (p.ncols + BN - 1) / BN;
     const int64_t tiles_m = (p.ph[0].M + BM - 1) / BM;
     p.ph[0].tiles_m = (int32_t)tiles_m;
     p.ph[0].block_start = 0;
-    const int64_t nb = tiles_m * p.tiles_n;
+    const int64_t nb = tiles_m * p.tiles_n * p.groups;
     if (nb <= 0) return hipSuccess;
     if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
     // 3x3 filters (the host admits no other tap count)
+    if constexpr (SINGLE) {
+        if (diag32) {
+            hipLaunchKernelGGL((igemm_hring_kernel<T, BM, BN, WM, WN, HR, HRING_TAPS, 3, NB, OCC, true>),
+                               dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
+            return hipGetLastError();
+        }
+    }
     hipLaunchKernelGGL((igemm_hring_kernel<T, BM, BN, WM, WN, HR, HRING_TAPS, 3, NB, OCC>), dim3((uint32_t)nb),
                        dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
@@ -352,32 +387,35 @@ hipError_t launch_hring_cfg(TNParams &p, hipStream_t st) {
 //            (within 128), 48 KB, two workgroups per CU: 64-channel
 //            reductions with at most 64 output columns per tile
 template <class T>
-hipError_t launch_hring_t(HaloConfig cfg, TNParams &p, hipStream_t st) {
+hipError_t launch_hring_t(HaloConfig cfg, TNParams &p, bool diag32, hipStream_t st) {
     switch (cfg) {
-        case HALO_R256x128: return launch_hring_cfg<T, 256, 128, 2, 2, 320>(p, st);
-        case HALO_R224x256: return launch_hring_cfg<T, 224, 256, 1, 4, 256>(p, st);
-        case HALO_R256x64S: return launch_hring_cfg<T, 256, 64, 4, 1, 384, 1, 2>(p, st);
+        case HALO_R256x128: return launch_hring_cfg<T, 256, 128, 2, 2, 320>(p, false, st);
+        case HALO_R224x256: return launch_hring_cfg<T, 224, 256, 1, 4, 256>(p, false, st);
+        case HALO_R256x64S: return launch_hring_cfg<T, 256, 64, 4, 1, 384, 1, 2>(p, diag32, st);
         case HALO_R128x256:
-        default: return launch_hring_cfg<T, 128, 256, 1, 4, 256>(p, st);
+        default: return launch_hring_cfg<T, 128, 256, 1, 4, 256>(p, false, st);
     }
 }
 
 }  // namespace
 
-bool hring_supported(const TNParams &p, int span) {
-    return halo_supported(p) && p.ph[0].tap_count == HRING_TAPS && halo_tap_span(p) <= span;
+bool hring_supported(const TNParams &p, int span, bool grouped) {
+    return halo_supported(p, grouped) && p.ph[0].tap_count == HRING_TAPS &&
+           halo_tap_span(p) <= span;
 }
 
-hipError_t launch_igemm_hring(int dtype, HaloConfig cfg, TNParams &p, void *pack,
+hipError_t launch_igemm_hring(int dtype, HaloConfig cfg, TNParams &p, void *pack, bool diag32,
                               hipStream_t st) {
-    if (!halo_cfg_supported(p, cfg)) return hipErrorInvalidValue;
+    if (!halo_cfg_supported(p, cfg) || !pack) return hipErrorInvalidValue;
+    const size_t pb = hring_pack_bytes(p.ncols, p.cr, p.groups);
+    if (pb > 0xFFFFFFFFu) return hipErrorInvalidValue;
     hipError_t e = launch_hring_pack(p, pack, st);
     if (e != hipSuccess) return e;
     TNParams q = p;
     q.b = pack;
-    q.b_bytes = (uint32_t)hring_pack_bytes(p.ncols, p.cr);
-    if (dtype == Half::id) return launch_hring_t<Half>(cfg, q, st);
-    return launch_hring_t<BFloat>(cfg, q, st);
+    q.b_bytes = (uint32_t)pb;
+    if (dtype == Half::id) return launch_hring_t<Half>(cfg, q, diag32, st);
+    return launch_hring_t<BFloat>(cfg, q, diag32, st);
 }
 
 }  // namespace nnconv

@@ -100,7 +100,9 @@ hipError_t launch_igemm_c64(int dtype, C64Config cfg, TNParams &p, bool pad, hip
 // Halo staging for stride-1 "same" geometries (igemm_halo.hip): single
 // phase, one group, cr % 64 == 0, A image of the output's size, at most 32
 // taps whose raster shifts span at most HALO_SPAN pixels (3x3 filters with
-// padding 1 on images up to 63 pixels wide).
+// padding 1 on images up to 63 pixels wide).  The single-slice
+// register-weight tile also takes groups of 64 reduction channels into 64
+// output columns (grouped convolution run as 64-channel super-groups).
 constexpr int HALO_SPAN = 128;
 enum HaloConfig { HALO_256x64 = 0,      // 4 waves of 64x64
                   HALO_256x128 = 1,     // 4 waves of 128x64
@@ -114,7 +116,9 @@ enum HaloConfig { HALO_256x64 = 0,      // 4 waves of 64x64
                                         // (cr == 64), two workgroups per CU
 // the register-weight configurations are the ones from HALO_R256x128 on
 inline bool hring_config(int cfg) { return cfg >= HALO_R256x128 && cfg <= HALO_R256x64S; }
-bool halo_supported(const TNParams &p);
+// grouped: also accept p.groups > 1 with groups of cr reduction channels
+// into ncols output columns, side by side in the A and output pixels
+bool halo_supported(const TNParams &p, bool grouped = false);
 // largest minus smallest raster shift of the taps of phase 0
 int halo_tap_span(const TNParams &p);
 // raster span of the taps the configuration's halo buffer holds
@@ -122,16 +126,22 @@ int halo_cfg_span(HaloConfig cfg);
 // whether configuration cfg runs p (geometry, tap count and span)
 bool halo_cfg_supported(const TNParams &p, HaloConfig cfg);
 // hipErrorInvalidValue when !halo_cfg_supported(p, cfg); `pack` is used by
-// the register-weight configurations only (see launch_igemm_hring)
-hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, hipStream_t st);
+// the register-weight configurations only (see launch_igemm_hring).  diag32:
+// the per-tap 64x64 weight blocks are block-diagonal in 32x32 blocks
+// (super-groups of groups of at most 32 channels); the single-slice tile then
+// skips the zero blocks, the others ignore it.
+hipError_t launch_igemm_halo(int dtype, HaloConfig cfg, TNParams &p, void *pack, bool diag32,
+                             hipStream_t st);
 // The register-weight halo tiles (igemm_hring.hip) take 3x3 filters (9
-// taps) only, HALO_R256x64S a single 64-channel slice (cr == 64) too.  They read the B operand packed in fragment order: `pack` is
-// caller-provided device memory of hring_pack_bytes(ncols, cr) bytes, which
+// taps) only, HALO_R256x64S a single 64-channel slice (cr == 64) too, and
+// it alone more than one group (each of 64 output columns).  They read the
+// B operand packed in fragment order: `pack` is caller-provided device
+// memory of hring_pack_bytes(ncols, cr, groups) bytes, which
 // launch_igemm_hring fills from p.b before the GEMM.
 constexpr int HRING_TAPS = 9;
-bool hring_supported(const TNParams &p, int span);
-size_t hring_pack_bytes(int64_t ncols, int64_t cr);
-hipError_t launch_igemm_hring(int dtype, HaloConfig cfg, TNParams &p, void *pack,
+bool hring_supported(const TNParams &p, int span, bool grouped = false);
+size_t hring_pack_bytes(int64_t ncols, int64_t cr, int64_t groups = 1);
+hipError_t launch_igemm_hring(int dtype, HaloConfig cfg, TNParams &p, void *pack, bool diag32,
                               hipStream_t st);
 
 // Forward pass for 8-channel (16-byte) channel-last pixels, 64 output

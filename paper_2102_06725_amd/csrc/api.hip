@@ -169,21 +169,23 @@ struct WgPlan {
 
 // Rows per block of the row-block backward-weight kernel (wgrad_halo.hip)
 // for this geometry, or 0 when it does not run it: 3x3 stride-1 "same"
-// convolutions (padding 1, dilation 1) of one group with 64 input and 64
-// output channels (not super-groups of smaller groups), on images whose
-// width admits blocks of whole rows of a multiple of 16 and at most 128
-// pixels (the largest such block is taken) that fits the kernel's LDS
-// buffers.
+// convolutions (padding 1, dilation 1) with groups of 64 input and 64 output
+// channels (super-groups of smaller groups included), on images whose width
+// admits blocks of whole rows of a multiple of 16 and at most 128 pixels
+// (the largest such block is taken) that fits the kernel's LDS buffers.
+// With more than one group the block may not be taller than the image (a
+// 7x7 image would stage 16-row blocks: the 64-row tiles do better there).
 int64_t wgh_rows(const Geom &G) {
-    if (!(G.g == 1 && !G.diag32 && G.cg == 64 && G.kg == 64 && G.r == 3 && G.s == 3 && G.sh == 1 &&
-          G.sw == 1 && G.dh == 1 && G.dw == 1 && G.ph == 1 && G.pw == 1 && G.p == G.h &&
-          G.q == G.w))
+    if (!(G.cg == 64 && G.kg == 64 && G.r == 3 && G.s == 3 && G.sh == 1 && G.sw == 1 &&
+          G.dh == 1 && G.dw == 1 && G.ph == 1 && G.pw == 1 && G.p == G.h && G.q == G.w &&
+          G.g <= 65535))
         return 0;
     int64_t rb0 = 1;
     while ((rb0 * G.w) % 16 != 0) ++rb0;  // at most 16
     if (rb0 * G.w > 128) return 0;
     const int64_t rb = rb0 * (128 / (rb0 * G.w));
     if (wgh_slots((int)rb, (int)G.w) > WGH_MAX_SLOTS) return 0;
+    if (G.g > 1 && rb > G.h) return 0;
     return rb;
 }
 
@@ -226,12 +228,12 @@ WgPlan plan_wgrad_fast(const Geom &G) {
     }
     pl.rb = (int32_t)wgh_rows(G);
     if (pl.rb > 0) {
-        // one workgroup per CU, consecutive row blocks each
+        // one workgroup per CU (over all groups), consecutive row blocks each
         pl.cfg = WG_HALO;
         pl.blocks_per_img = (int32_t)((G.h + pl.rb - 1) / pl.rb);
         const int64_t nb = G.n * pl.blocks_per_img;
         const int64_t cus = device_cus();
-        const int64_t per = (nb + cus - 1) / cus;
+        const int64_t per = (nb * G.g + cus - 1) / cus;
         pl.nblocks = (int32_t)nb;
         pl.blocks_per_split = (int32_t)per;
         pl.splits = (int32_t)((nb + per - 1) / per);
@@ -836,6 +838,8 @@ nnconv_status wgrad_fast(const Geom &G, const void *x, const void *dy, float *pa
         hp.nblocks = pl.nblocks;
         hp.blocks_per_split = pl.blocks_per_split;
         hp.splits = pl.splits;
+        hp.groups = (int32_t)G.g;
+        hp.diag32 = G.diag32;
         TRY_HIP(launch_wgrad_halo(G.dtype, hp, st));
         return NNCONV_OK;
     }

@@ -197,11 +197,15 @@ enum WGConfig { WG_128x128 = 0, WG_64x128 = 1, WG_256x256 = 2, WG_128x128S = 3,
 // Pixel ranges of pix_per_split (a multiple of 32) pixels each.
 hipError_t launch_wgrad_splitk(int dtype, WGConfig cfg, WGParams &p, hipStream_t st);
 
-// Backward-weight of a 3x3 stride-1 convolution with padding 1, one group,
+// Backward-weight of a 3x3 stride-1 convolution with padding 1 and groups of
 // 64 input and 64 output channels (wgrad_halo.hip): blocks of rb whole image
 // rows (rb * w a multiple of 16, at most 128 pixels, wgh_slots(rb, w) at
 // most WGH_MAX_SLOTS), blocks_per_split consecutive blocks per workgroup,
-// each workgroup writing ws[split][64][9 * 64] (fp32, columns (tap, c)).
+// workgroup (split, group) writing rows group * 64 .. + 63 of
+// ws[split][groups * 64][9 * 64] (fp32, columns (tap, c)).  diag32: the
+// groups are super-groups of groups of at most 32 channels, whose gradient
+// is block-diagonal in 32x32 blocks: only those blocks are computed and
+// written (the rest of each row is left as it was).
 constexpr int WGH_MAX_SLOTS = 3392;
 // 16-byte LDS slots a block of rb rows of a w-wide image stages
 int wgh_slots(int rb, int w);
@@ -213,6 +217,8 @@ struct WGHParams {
     int32_t h, w;                  // image size (input = output)
     int32_t c_stride, k_stride;    // channels per pixel of x and dy
     int32_t rb, blocks_per_img, nblocks, blocks_per_split, splits;
+    int32_t groups;                // of 64 channels, side by side in x and dy pixels
+    int32_t diag32;
 };
 hipError_t launch_wgrad_halo(int dtype, const WGHParams &p, hipStream_t st);
 

@@ -1,6 +1,7 @@
 // wgrad_halo.hip -- backward-weight pass of 3x3 stride-1 "same" convolutions
 // with 64 input and 64 output channels per group (the 56x56 3x3 layers of
-// ResNet-50's first stage), without an im2col.
+// ResNet-50's first stage, and the 64-channel super-groups of grouped
+// layers), without an im2col.
 //
 //   part[split][k][t * 64 + c] = sum over the split's pixels p of
 //                                dy[p][k] * x[p + shift(t)][c]   (zero outside the image)
@@ -86,8 +87,11 @@ __device__ __forceinline__ u32x4 tr_frag(uint32_t a0, uint32_t a1) {
 }  // namespace wgh
 
 // WAVES waves (4: taps 0-4 / 5-8 per wave, 8: {0, 1, 2}, {3, 4}, {5, 6},
-// {7, 8}), NBUF block buffers in LDS (NBUF - 1 blocks in flight).
-template <class T, int WAVES, int NBUF>
+// {7, 8}), NBUF block buffers in LDS (NBUF - 1 blocks in flight).  Group
+// blockIdx.y of 64 channels.  DIAG: block-diagonal 32x32 gradient blocks
+// (super-groups of groups of at most 32 channels): a wave computes only the
+// 32-row half of the output channels that matches its 32 input channels.
+template <class T, int WAVES, int NBUF, bool DIAG>
 __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHParams P) {
     using namespace wgh;
     static_assert(WAVES == 4 || WAVES == 8, "tap groups");
@@ -104,6 +108,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void *)&lds[0];
     const i32x4 ddy = desc_of(P.dy, P.dy_bytes);
     const i32x4 dx = desc_of(P.x, P.x_bytes);
+    const int grp = (int)blockIdx.y;
+    const uint32_t goff = (uint32_t)grp * 128u;  // the group's 64 channels, in bytes
 
     const int W = P.w, H = P.h, RB = P.rb, W2 = P.w + 2;
     const int npix = RB * W;          // pixels per block, a multiple of 16
@@ -168,11 +174,13 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
                 const bool ok = (pk[j] >> 31) != 0 && (unsigned)ih < (unsigned)H;
                 if (e0 < dys) {
                     const uint32_t off =
-                        ok ? (uint32_t)(pix0 + rel) * (uint32_t)P.k_stride * 2u + chb : OOB_OFFSET;
+                        ok ? (uint32_t)(pix0 + rel) * (uint32_t)P.k_stride * 2u + goff + chb
+                           : OOB_OFFSET;
                     dma16(base + (uint32_t)e0 * 16u, off, ddy);
                 } else {
                     const uint32_t off =
-                        ok ? (uint32_t)(pix0 + rel) * (uint32_t)P.c_stride * 2u + chb : OOB_OFFSET;
+                        ok ? (uint32_t)(pix0 + rel) * (uint32_t)P.c_stride * 2u + goff + chb
+                           : OOB_OFFSET;
                     dma16(base + (uint32_t)e0 * 16u, off, dx);
                 }
             }
@@ -188,6 +196,10 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
     const uint32_t fr_col = (uint32_t)(16 * (gq & 1) + 4 * (li & 3)) * 2u;
     const int cb = wave & 1;          // input-channel block of this wave
     const int tg = wave >> 1;         // tap group
+    // output-channel halves of this wave: both, or (DIAG) the one of its
+    // input-channel block
+    constexpr int NI = DIAG ? 1 : 2;
+    auto half = [&](int i) { return DIAG ? cb : i; };
     // staged input position of pixel p's centre, in bytes: (p / W + 1) rows
     // of W + 2 pixels, column p % W + 1
     uint32_t xpos[MAXKS][2];
@@ -203,9 +215,9 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
     // tap t = (dh + 1) * 3 + (dw + 1): byte offset of its input pixel
     auto tap_off = [&](int t) -> int { return ((t / 3 - 1) * W2 + (t % 3 - 1)) * PITCH; };
 
-    f32x16 acc[2][NTMAX];
+    f32x16 acc[NI][NTMAX];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
         for (int t = 0; t < NTMAX; ++t) acc[i][t] = f32x16{};
     // wave-uniform tap offsets, kept in scalar registers
@@ -216,12 +228,13 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
     // the k-steps of one staged block, taps T0 .. T0 + NT - 1
     auto block = [&](const uint32_t base, auto t0c, auto ntc) {
         constexpr int T0 = decltype(t0c)::value, NT = decltype(ntc)::value;
-        // the fragments of k-step ks: two of dy (both 32-row halves of the
-        // output channels), one of the staged input per tap
-        auto read = [&](int ks, u32x4 (&fa)[2], u32x4 (&fb)[NT]) {
+        // the fragments of k-step ks: NI of dy (the wave's 32-row halves of
+        // the output channels), one of the staged input per tap
+        auto read = [&](int ks, u32x4 (&fa)[NI], u32x4 (&fb)[NT]) {
             const uint32_t a = base + (uint32_t)((ks * 16 + fr_row) * PITCH) + fr_col;
 #pragma unroll
-            for (int i = 0; i < 2; ++i) fa[i] = tr_frag(a + i * 64, a + i * 64 + 4 * PITCH);
+            for (int i = 0; i < NI; ++i)
+                fa[i] = tr_frag(a + half(i) * 64, a + half(i) * 64 + 4 * PITCH);
             // the pixel positions of this k-step, opaque to the compiler:
             // otherwise it keeps every (k-step, tap) address in registers
             uint32_t x0 = base + xpos[ks][0], x1 = base + xpos[ks][1];
@@ -232,7 +245,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
         // each k-step's fragments are read before the previous k-step's
         // matrix-core instructions issue (the fences keep that order and
         // keep the compiler from reading further ahead)
-        u32x4 fa[2][2], fb[2][NT];
+        u32x4 fa[2][NI], fb[2][NT];
         read(0, fa[0], fb[0]);
 #pragma unroll
         for (int ks = 0; ks < MAXKS; ++ks) {
@@ -243,7 +256,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
 #pragma unroll
-                    for (int i = 0; i < 2; ++i) acc[i][t] = mfma32<T>(fa[cur][i], fb[cur][t], acc[i][t]);
+                    for (int i = 0; i < NI; ++i) acc[i][t] = mfma32<T>(fa[cur][i], fb[cur][t], acc[i][t]);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -287,11 +300,12 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
         buf = buf == NBUF - 1 ? 0 : buf + 1;
     }
 
-    // partial [64 k][9 * 64]: lane holds column l32 of its 32-channel block
-    // and rows 8 * (v / 4) + 4 * (lane / 32) + v % 4 of each 32-row half
+    // partial rows grp * 64 .. + 63 of [groups * 64 k][9 * 64]: lane holds
+    // column l32 of its 32-channel block and rows 8 * (v / 4) + 4 * (lane /
+    // 32) + v % 4 of each of its 32-row halves
     const int l32 = lane & 31, kh = lane >> 5;
     constexpr int NCOL = 9 * 64;
-    float *dst = P.ws + (int64_t)blockIdx.x * 64 * NCOL;
+    float *dst = P.ws + ((int64_t)blockIdx.x * P.groups + grp) * 64 * NCOL;
     const int t0 = NG == 2 ? 5 * tg : (tg == 0 ? 0 : 2 * tg + 1);
     const int nt = NG == 2 ? (tg == 0 ? 5 : 4) : (tg == 0 ? 3 : 2);
 #pragma unroll
@@ -299,10 +313,10 @@ __global__ __launch_bounds__(WAVES * 64, 1) void wgrad_halo_kernel(const WGHPara
         if (t < nt) {
             const int col = (t0 + t) * 64 + cb * 32 + l32;
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < NI; ++i)
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
-                    dst[(32 * i + 8 * (v >> 2) + 4 * kh + (v & 3)) * NCOL + col] = acc[i][t][v];
+                    dst[(32 * half(i) + 8 * (v >> 2) + 4 * kh + (v & 3)) * NCOL + col] = acc[i][t][v];
         }
     }
 }
@@ -314,16 +328,26 @@ int wgh_slots(int rb, int w) {
 
 hipError_t launch_wgrad_halo(int dtype, const WGHParams &p, hipStream_t st) {
     if (p.rb < 1 || p.w < 1 || p.rb * p.w > wgh::MAXP || (p.rb * p.w) % 16 != 0 ||
-        wgh_slots(p.rb, p.w) > WGH_MAX_SLOTS || p.blocks_per_split < 1 || p.splits < 1)
+        wgh_slots(p.rb, p.w) > WGH_MAX_SLOTS || p.blocks_per_split < 1 || p.splits < 1 ||
+        p.groups < 1 || p.groups > 65535 || p.c_stride < 64 * p.groups ||
+        p.k_stride < 64 * p.groups)
         return hipErrorInvalidValue;
     // 8 waves and 3 buffers: on the 56x56 layer at batch 256, 86 us against
     // 87 with 2 buffers and 117-120 with 4 waves (one per SIMD does not hide
     // the transposing reads' latency)
     constexpr int WV = 8, NB = 3;
-    if (dtype == Half::id)
-        hipLaunchKernelGGL((wgrad_halo_kernel<Half, WV, NB>), dim3(p.splits), dim3(WV * 64), 0, st, p);
-    else
-        hipLaunchKernelGGL((wgrad_halo_kernel<BFloat, WV, NB>), dim3(p.splits), dim3(WV * 64), 0, st, p);
+    const dim3 grid((uint32_t)p.splits, (uint32_t)p.groups);
+    if (dtype == Half::id) {
+        if (p.diag32)
+            hipLaunchKernelGGL((wgrad_halo_kernel<Half, WV, NB, true>), grid, dim3(WV * 64), 0, st, p);
+        else
+            hipLaunchKernelGGL((wgrad_halo_kernel<Half, WV, NB, false>), grid, dim3(WV * 64), 0, st, p);
+    } else {
+        if (p.diag32)
+            hipLaunchKernelGGL((wgrad_halo_kernel<BFloat, WV, NB, true>), grid, dim3(WV * 64), 0, st, p);
+        else
+            hipLaunchKernelGGL((wgrad_halo_kernel<BFloat, WV, NB, false>), grid, dim3(WV * 64), 0, st, p);
+    }
     return hipGetLastError();
 }
 

@@ -162,6 +162,17 @@ SMALL = [
     ("groups 32 x 4 channels stride 3", Case(L("sg4s3", 2, 128, 10, 11, 128, 3, 3, 3, 1,
                                                 groups=32))),
     ("depthwise 3x5 as super-groups", Case(L("sg1", 2, 64, 7, 8, 64, 3, 5, 1, 1, groups=64))),
+    # stride-1 3x3 super-groups on a 56-wide image: two 256-row halo tiles
+    # per group, row blocks of 2 rows for backward-weight (the last one short)
+    ("groups 32 x 4 channels 56 wide", Case(L("sg4w", 1, 128, 5, 56, 128, 3, 3, 1, 1,
+                                                groups=32))),
+    ("groups 16 x 4 channels dilation 2", Case(L("sg4d", 2, 64, 12, 13, 64, 3, 3, 1, 2, dil=2,
+                                                   groups=16))),
+    # groups of exactly 64 channels: the halo tiles' group mode without the
+    # block-diagonal skip (row blocks of 8 rows, the last one short)
+    ("groups 2 x 64 channels", Case(L("g64", 2, 128, 11, 16, 128, 3, 3, 1, 1, groups=2))),
+    ("groups 3 x 64 channels NCHW bf16", Case(L("g64b", 2, 192, 9, 12, 192, 3, 3, 1, 1,
+                                                  groups=3), layout="nchw", dtype=I.BF16)),
     ("direct: depthwise 3x5", Case(L("dw10", 2, 16, 8, 9, 16, 3, 5, 1, 1, groups=16))),
 ]
 

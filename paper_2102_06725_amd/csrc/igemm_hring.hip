@@ -347,7 +347,7 @@ hipError_t launch_hring_pack(const TNParams &p, void *dst, hipStream_t st) {
 
 namespace {
 
-template <class T, int BM, int BN, int WM, int WN, int HR, int NB = 2, int OCC = 1>
+template <class T, int BM, int BN, int WM, int WN, int HR, int NB = 2, int OCC = 1, int D = 3>
 hipError_t launch_hring_cfg(TNParams &p, bool diag32, hipStream_t st) {
     // groups (of 64 channels into 64 columns) and block-diagonal weights on
     // the single-slice tile only
@@ -365,12 +365,13 @@ hipError_t launch_hring_cfg(TNParams &p, bool diag32, hipStream_t st) {
     // 3x3 filters (the host admits no other tap count)
     if constexpr (SINGLE) {
         if (diag32) {
+            // half the weight fragments: three steps of them fit in flight
             hipLaunchKernelGGL((igemm_hring_kernel<T, BM, BN, WM, WN, HR, HRING_TAPS, 3, NB, OCC, true>),
                                dim3((uint32_t)nb), dim3(WM * WN * 64), 0, st, p);
             return hipGetLastError();
         }
     }
-    hipLaunchKernelGGL((igemm_hring_kernel<T, BM, BN, WM, WN, HR, HRING_TAPS, 3, NB, OCC>), dim3((uint32_t)nb),
+    hipLaunchKernelGGL((igemm_hring_kernel<T, BM, BN, WM, WN, HR, HRING_TAPS, D, NB, OCC>), dim3((uint32_t)nb),
                        dim3(WM * WN * 64), 0, st, p);
     return hipGetLastError();
 }
@@ -384,14 +385,17 @@ hipError_t launch_hring_cfg(TNParams &p, bool diag32, hipStream_t st) {
 //            up to 15 wide), 64 KB; 224 tiles for the 14x14 3x3 layers at
 //            batch 256: one round on 256 CUs
 //   256x64 single slice: 4 waves of 64x64, one halo buffer of 384 rows
-//            (within 128), 48 KB, two workgroups per CU: 64-channel
+//            (within 128), 48 KB, three workgroups per CU (the weight
+//            fragments loaded one step ahead, 134 registers: three steps
+//            ahead need 207, two workgroups; s2b0b forward / backward-data
+//            in the sweep 88 / 93 -> 85 / 90 us): 64-channel
 //            reductions with at most 64 output columns per tile
 template <class T>
 hipError_t launch_hring_t(HaloConfig cfg, TNParams &p, bool diag32, hipStream_t st) {
     switch (cfg) {
         case HALO_R256x128: return launch_hring_cfg<T, 256, 128, 2, 2, 320>(p, false, st);
         case HALO_R224x256: return launch_hring_cfg<T, 224, 256, 1, 4, 256>(p, false, st);
-        case HALO_R256x64S: return launch_hring_cfg<T, 256, 64, 4, 1, 384, 1, 2>(p, diag32, st);
+        case HALO_R256x64S: return launch_hring_cfg<T, 256, 64, 4, 1, 384, 1, 3, 1>(p, diag32, st);
         case HALO_R128x256:
         default: return launch_hring_cfg<T, 128, 256, 1, 4, 256>(p, false, st);
     }

@@ -113,7 +113,7 @@ enum HaloConfig { HALO_256x64 = 0,      // 4 waves of 64x64
                   HALO_R128x256 = 4,    // 4 waves of 128x64 side by side, taps within 128
                   HALO_R224x256 = 5,    // 4 waves of 224x64 side by side, taps within 32
                   HALO_R256x64S = 6 };  // 4 waves of 64x64, single 64-channel slice
-                                        // (cr == 64), two workgroups per CU
+                                        // (cr == 64), three workgroups per CU
 // the register-weight configurations are the ones from HALO_R256x128 on
 inline bool hring_config(int cfg) { return cfg >= HALO_R256x128 && cfg <= HALO_R256x64S; }
 // grouped: also accept p.groups > 1 with groups of cr reduction channels
